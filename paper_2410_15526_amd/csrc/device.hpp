@@ -1,0 +1,306 @@
+// device.hpp -- wavefront building blocks shared by the gfx950 kernels.
+//
+// Register layout used by every element-wise kernel: a wavefront owns a
+// "wave tile" of 64*E consecutive elements and lane l holds the E
+// consecutive elements [E*l, E*l + E) of it.  Quantization groups and
+// Hadamard blocks are aligned to E-element lane slices (group >= E), so a
+// group or block is either inside one lane (handled in registers) or spans
+// 2^k neighbouring lanes (handled with cross-lane exchanges).
+//
+// Global memory is read and written in the coalesced order (instruction i,
+// lane l touches the 16-byte chunk 64*i + l of the tile) and transposed to
+// or from the lane-contiguous layout through a wave-private LDS region, with
+// an XOR swizzle of the chunk index so that both the coalesced and the
+// transposed access patterns are free of LDS bank conflicts.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define SDP4_DEV __device__ __forceinline__
+
+namespace sdp4 {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kBlockThreads = 256;
+constexpr int kWavesPerBlock = kBlockThreads / kWave;
+
+SDP4_DEV int lane_id() { return __lane_id(); }
+
+// Order LDS traffic of one wavefront: everything before is visible to every
+// lane of the wave after, and the compiler does not move memory ops across.
+SDP4_DEV void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// ---------------------------------------------------------------------------
+// cross-lane exchange: value of lane (lane ^ D)
+// ---------------------------------------------------------------------------
+template <int D>
+SDP4_DEV float xor_lane(float v)
+{
+    static_assert(D == 1 || D == 2 || D == 4 || D == 8 || D == 16 || D == 32, "distance");
+    const int iv = __builtin_bit_cast(int, v);
+    int r;
+    if constexpr (D == 1) {
+        r = __builtin_amdgcn_mov_dpp(iv, 0xB1, 0xF, 0xF, true); // quad_perm [1,0,3,2]
+    } else if constexpr (D == 2) {
+        r = __builtin_amdgcn_mov_dpp(iv, 0x4E, 0xF, 0xF, true); // quad_perm [2,3,0,1]
+    } else if constexpr (D < 32) {
+        r = __builtin_amdgcn_ds_swizzle(iv, (D << 10) | 0x1F); // bit mode: lane ^ D within 32
+    } else {
+        r = __builtin_amdgcn_ds_bpermute((lane_id() ^ 32) << 2, iv);
+    }
+    return __builtin_bit_cast(float, r);
+}
+
+template <int E>
+SDP4_DEV void max_lanes(float &a, int lanes)
+{
+    // reduce over `lanes` (power of two, 1..64) neighbouring lanes
+    if (lanes > 1) a = fmaxf(a, xor_lane<1>(a));
+    if (lanes > 2) a = fmaxf(a, xor_lane<2>(a));
+    if (lanes > 4) a = fmaxf(a, xor_lane<4>(a));
+    if (lanes > 8) a = fmaxf(a, xor_lane<8>(a));
+    if (lanes > 16) a = fmaxf(a, xor_lane<16>(a));
+    if (lanes > 32) a = fmaxf(a, xor_lane<32>(a));
+}
+
+SDP4_DEV void minmax_lanes(float &mn, float &mx, int lanes)
+{
+    if (lanes > 1) { mn = fminf(mn, xor_lane<1>(mn)); mx = fmaxf(mx, xor_lane<1>(mx)); }
+    if (lanes > 2) { mn = fminf(mn, xor_lane<2>(mn)); mx = fmaxf(mx, xor_lane<2>(mx)); }
+    if (lanes > 4) { mn = fminf(mn, xor_lane<4>(mn)); mx = fmaxf(mx, xor_lane<4>(mx)); }
+    if (lanes > 8) { mn = fminf(mn, xor_lane<8>(mn)); mx = fmaxf(mx, xor_lane<8>(mx)); }
+    if (lanes > 16) { mn = fminf(mn, xor_lane<16>(mn)); mx = fmaxf(mx, xor_lane<16>(mx)); }
+    if (lanes > 32) { mn = fminf(mn, xor_lane<32>(mn)); mx = fmaxf(mx, xor_lane<32>(mx)); }
+}
+
+// ---------------------------------------------------------------------------
+// LDS staging between the coalesced and the lane-contiguous layouts
+// ---------------------------------------------------------------------------
+// R = 16-byte chunks per lane; the wave tile has 64*R chunks.
+template <int R>
+SDP4_DEV int swz(int c)
+{
+    if constexpr (R >= 8)
+        return c ^ ((c / R) & 7);
+    else
+        return c ^ ((c >> 3) & 7);
+}
+
+// Global (coalesced) -> registers (lane-contiguous).  Chunks at or beyond
+// `valid` are not read and come back as zero.
+template <int R>
+SDP4_DEV void stage_in(const u32x4 *__restrict__ g, int valid, u32x4 *lds, u32x4 (&out)[R])
+{
+    const int lane = lane_id();
+    u32x4 t[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int c = kWave * i + lane;
+        t[i] = c < valid ? __builtin_nontemporal_load(g + c) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+        lds[swz<R>(kWave * i + lane)] = t[i];
+    wave_lds_sync();
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+        out[k] = lds[swz<R>(R * lane + k)];
+    wave_lds_sync();
+}
+
+// Registers (lane-contiguous) -> global (coalesced).  Chunks at or beyond
+// `valid` are not written.
+template <int R>
+SDP4_DEV void stage_out(u32x4 *__restrict__ g, int valid, u32x4 *lds, const u32x4 (&in)[R])
+{
+    const int lane = lane_id();
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+        lds[swz<R>(R * lane + k)] = in[k];
+    wave_lds_sync();
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int c = kWave * i + lane;
+        const u32x4 t = lds[swz<R>(c)];
+        if (c < valid)
+            __builtin_nontemporal_store(t, g + c);
+    }
+    wave_lds_sync();
+}
+
+template <int E>
+SDP4_DEV void chunks_to_f32(const u32x4 (&c)[E / 4], float (&v)[E])
+{
+#pragma unroll
+    for (int k = 0; k < E / 4; ++k) {
+        v[4 * k + 0] = __uint_as_float(c[k].x);
+        v[4 * k + 1] = __uint_as_float(c[k].y);
+        v[4 * k + 2] = __uint_as_float(c[k].z);
+        v[4 * k + 3] = __uint_as_float(c[k].w);
+    }
+}
+
+template <int E>
+SDP4_DEV void f32_to_chunks(const float (&v)[E], u32x4 (&c)[E / 4])
+{
+#pragma unroll
+    for (int k = 0; k < E / 4; ++k)
+        c[k] = u32x4{__float_as_uint(v[4 * k]), __float_as_uint(v[4 * k + 1]),
+                     __float_as_uint(v[4 * k + 2]), __float_as_uint(v[4 * k + 3])};
+}
+
+// bfloat16 pairs (E/8 chunks) <-> float
+template <int E>
+SDP4_DEV void bf16_chunks_to_f32(const u32x4 (&c)[E / 8], float (&v)[E])
+{
+#pragma unroll
+    for (int k = 0; k < E / 8; ++k) {
+        const uint32_t w[4] = {c[k].x, c[k].y, c[k].z, c[k].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[8 * k + 2 * j] = __uint_as_float(w[j] << 16);
+            v[8 * k + 2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+        }
+    }
+}
+
+// float -> bfloat16 bits, round to nearest even (finite inputs)
+SDP4_DEV uint32_t bf16_rne_bits(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+template <int E>
+SDP4_DEV void f32_to_bf16_chunks(const float (&v)[E], u32x4 (&c)[E / 8])
+{
+#pragma unroll
+    for (int k = 0; k < E / 8; ++k) {
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            w[j] = bf16_rne_bits(v[8 * k + 2 * j]) | (bf16_rne_bits(v[8 * k + 2 * j + 1]) << 16);
+        c[k] = u32x4{w[0], w[1], w[2], w[3]};
+    }
+}
+
+// ---------------------------------------------------------------------------
+// blockwise Hadamard transform on the lane layout
+// ---------------------------------------------------------------------------
+// Butterfly stages of width h = 1, 2, ..., nblk/2 in that order, then one
+// multiplication by cn.  Widths below E pair registers of one lane; width
+// h >= E pairs register i of lane l with register i of lane l ^ (h / E):
+// the lower lane keeps a + b and the upper one a - b, both computed as a
+// single-rounding fma(own, +-1, other).
+template <int E, int D>
+SDP4_DEV void fwht_cross(float (&v)[E])
+{
+    const float sg = (lane_id() & D) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+        const float p = xor_lane<D>(v[i]);
+        v[i] = __builtin_fmaf(v[i], sg, p);
+    }
+}
+
+template <int E>
+SDP4_DEV void fwht_lane(float (&v)[E], int nblk, float cn)
+{
+#pragma unroll
+    for (int h = 1; h < E; h <<= 1) {
+        if (h < nblk) {
+#pragma unroll
+            for (int i = 0; i < E; ++i) {
+                if (i & h)
+                    continue;
+                const float a = v[i], b = v[i + h];
+                v[i] = a + b;
+                v[i + h] = a - b;
+            }
+        }
+    }
+    if (nblk > E) fwht_cross<E, 1>(v);
+    if (nblk > 2 * E) fwht_cross<E, 2>(v);
+    if (nblk > 4 * E) fwht_cross<E, 4>(v);
+    if (nblk > 8 * E) fwht_cross<E, 8>(v);
+    if (nblk > 16 * E) fwht_cross<E, 16>(v);
+    if (nblk > 32 * E) fwht_cross<E, 32>(v);
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+        v[i] = v[i] * cn;
+}
+
+// ---------------------------------------------------------------------------
+// quantize and pack
+// ---------------------------------------------------------------------------
+// Per-group symmetric parameters from the group's largest magnitude `a`.
+SDP4_DEV void sym_params(float a, float qmax, float &scale, float &inv)
+{
+    const float r = qmax / a;
+    const bool degenerate = !(a > 0.0f) || !__builtin_isfinite(r);
+    scale = degenerate ? 0.0f : a / qmax;
+    inv = degenerate ? 0.0f : r;
+}
+
+SDP4_DEV int quant_sym1(float x, float inv, float qmax)
+{
+    const float r = __builtin_rintf(x * inv);
+    return (int)__builtin_amdgcn_fmed3f(r, -qmax, qmax);
+}
+
+// E codes -> E bytes (int8) as E/16 chunks
+template <int E>
+SDP4_DEV void pack8(const int (&q)[E], u32x4 (&c)[E / 16])
+{
+#pragma unroll
+    for (int k = 0; k < E / 16; ++k) {
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int *p = q + 16 * k + 4 * j;
+            w[j] = (uint32_t)(p[0] & 0xFF) | ((uint32_t)(p[1] & 0xFF) << 8) |
+                   ((uint32_t)(p[2] & 0xFF) << 16) | ((uint32_t)p[3] << 24);
+        }
+        c[k] = u32x4{w[0], w[1], w[2], w[3]};
+    }
+}
+
+// E codes -> E/2 bytes (nibbles, even element low) as E/32 chunks
+template <int E>
+SDP4_DEV void pack4(const int (&q)[E], u32x4 (&c)[E / 32])
+{
+#pragma unroll
+    for (int k = 0; k < E / 32; ++k) {
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint32_t acc = 0;
+#pragma unroll
+            for (int m = 0; m < 8; ++m)
+                acc |= (uint32_t)(q[32 * k + 8 * j + m] & 0xF) << (4 * m);
+            w[j] = acc;
+        }
+        c[k] = u32x4{w[0], w[1], w[2], w[3]};
+    }
+}
+
+// signed code e of a chunk array holding `bits`-wide codes
+template <int BITS>
+SDP4_DEV float code_f(const uint32_t *w, int e)
+{
+    if constexpr (BITS == 8)
+        return (float)((int32_t)(w[e >> 2] << (24 - 8 * (e & 3))) >> 24);
+    else
+        return (float)((int32_t)(w[e >> 3] << (28 - 4 * (e & 7))) >> 28);
+}
+
+} // namespace sdp4

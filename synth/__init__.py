@@ -183,28 +183,43 @@ def scaled(w: Workload, n: int) -> Workload:
 # weights (qWD inputs)
 # ----------------------------------------------------------------------------
 
+def _prev_chunk(w: Workload, seed: int, c: int) -> np.ndarray:
+    x = _rng(seed, w.wid, STREAM_PREV, c).standard_normal(CHUNK, dtype=np.float32)
+    x *= np.float32(w.weight_sigma)
+    return bf16_bits_toward_zero(x) if w.prev_dtype == "bf16" else x
+
+
+def _diff_chunk(w: Workload, seed: int, c: int) -> np.ndarray:
+    r = _rng(seed, w.wid, STREAM_DIFF, c)
+    z = r.standard_normal(CHUNK, dtype=np.float32)
+    if w.diff_kind != "normal":
+        # Student-t(3) rescaled to unit variance: Z / sqrt(2 Gamma(3/2))
+        g = r.standard_gamma(1.5, CHUNK, dtype=np.float32)
+        np.maximum(g, np.float32(1e-30), out=g)
+        g *= np.float32(2.0)
+        np.sqrt(g, out=g)
+        z /= g
+    z *= np.float32(w.diff_sigma)
+    return z
+
+
 def prev_weights(w: Workload, start: int, count: int, seed: int = 0) -> np.ndarray:
     """Previously communicated model weights: float32, or bfloat16 bits (uint16)."""
-    x = standard_normal(seed, w.wid, STREAM_PREV, start, count) * np.float32(w.weight_sigma)
-    if w.prev_dtype == "bf16":
-        return bf16_bits_toward_zero(x)
-    return x
+    dt = np.uint16 if w.prev_dtype == "bf16" else np.float32
+    return _chunked(lambda c: _prev_chunk(w, seed, c), start, count, dt)
 
 
 def weight_diff(w: Workload, start: int, count: int, seed: int = 0) -> np.ndarray:
-    if w.diff_kind == "normal":
-        z = standard_normal(seed, w.wid, STREAM_DIFF, start, count)
-    else:
-        z = student_t3_unit(seed, w.wid, STREAM_DIFF, start, count)
-    return z * np.float32(w.diff_sigma)
+    return _chunked(lambda c: _diff_chunk(w, seed, c), start, count, np.float32)
 
 
 def new_weights(w: Workload, start: int, count: int, seed: int = 0, prev: np.ndarray | None = None) -> np.ndarray:
     """fp32 main weights = previous weights (widened) + a synthetic update."""
-    if prev is None:
-        prev = prev_weights(w, start, count, seed)
-    base = bf16_bits_to_f32(prev) if w.prev_dtype == "bf16" else prev
-    return (base + weight_diff(w, start, count, seed)).astype(np.float32)
+    def chunk(c: int) -> np.ndarray:
+        p = _prev_chunk(w, seed, c)
+        base = bf16_bits_to_f32(p) if w.prev_dtype == "bf16" else p
+        return base + _diff_chunk(w, seed, c)
+    return _chunked(chunk, start, count, np.float32)
 
 
 # ----------------------------------------------------------------------------
@@ -237,14 +252,18 @@ def _gradient_chunk(w: Workload, seed: int, stream: int, c: int) -> np.ndarray:
         return z
     sig, chans = _layer_layout(w, seed)
     n_layers = len(sig)
-    idx = np.arange(c * CHUNK, (c + 1) * CHUNK, dtype=np.int64)
-    layer = np.minimum(idx // w.layer_elems, n_layers - 1)
-    out = z * sig[layer]
-    chan = (idx - layer * w.layer_elems) % w.hidden
-    for l in np.unique(layer):
-        m = (layer == l) & np.isin(chan, chans[l])
-        out[m] *= np.float32(w.outlier_mult)
-    return out
+    lo = c * CHUNK
+    while lo < (c + 1) * CHUNK:                      # a chunk spans at most a few layers
+        layer = min(lo // w.layer_elems, n_layers - 1)
+        end = min((c + 1) * CHUNK, (layer + 1) * w.layer_elems if layer < n_layers - 1 else (c + 1) * CHUNK)
+        seg = z[lo - c * CHUNK:end - c * CHUNK]
+        seg *= sig[layer]
+        mask = np.zeros(w.hidden, dtype=bool)
+        mask[chans[layer]] = True
+        off = (lo - layer * w.layer_elems) % w.hidden
+        seg[np.resize(np.roll(mask, -off), seg.size)] *= np.float32(w.outlier_mult)
+        lo = end
+    return z
 
 
 def gradient(w: Workload, start: int, count: int, seed: int = 0, peer: int | None = None) -> np.ndarray:

@@ -1,0 +1,157 @@
+"""The C ABI library on a host without a GPU: it loads, exports every entry
+point the public header declares, and rejects invalid arguments on the
+host with the documented status before anything reaches the device (these
+calls never launch a kernel)."""
+import ctypes as C
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2410_15526_amd import sdp4
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sdp4.h")
+
+OK, EINVAL, EALIGN, ERANGE = 0, 1, 2, 3
+A = 0x7F0000000000          # fake, 256-byte-aligned device addresses (never dereferenced)
+B = A + (1 << 32)
+CC = A + (2 << 32)
+D = A + (3 << 32)
+
+
+def declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(sdp4_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared()
+    assert "sdp4_qwd_encode" in names and "sdp4_dequant_reduce" in names
+    L = sdp4.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", sdp4._LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (sdp4_\w+)", out))
+    assert set(names) <= exported, set(names) - exported
+
+
+def test_helpers():
+    L = sdp4.lib()
+    assert L.sdp4_codes_bytes(1000, 4) == 500 and L.sdp4_codes_bytes(1000, 8) == 1000
+    assert L.sdp4_codes_bytes(1000, 3) == -1
+    assert L.sdp4_num_groups(4096, 128) == 32 and L.sdp4_num_groups(4096, 48) == -1
+    assert L.sdp4_num_groups(4096, 16) == -1 and L.sdp4_num_groups(4096, 8192) == -1
+    for s in range(5):
+        assert L.sdp4_status_string(s)
+    assert b"gfx950" in L.sdp4_version()
+    assert L.sdp4_last_hip_error() == 0
+
+
+def gq(x=A, n=4096, bits=8, block=256, group=128, codes=B, scale=CC):
+    return sdp4.lib().sdp4_grad_quant(x, n, bits, block, group, codes, scale, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(bits=3), EINVAL), (dict(bits=2), EINVAL), (dict(group=48), EINVAL), (dict(group=16), EINVAL),
+    (dict(group=8192), EINVAL), (dict(block=3), EINVAL), (dict(block=2048), EINVAL), (dict(block=1), EINVAL),
+    (dict(n=-128), EINVAL), (dict(n=100), EALIGN), (dict(n=128, block=256), EALIGN),
+    (dict(n=4096 + 128, group=256, block=0), EALIGN),
+    (dict(x=None), EINVAL), (dict(codes=None), EINVAL), (dict(scale=None), EINVAL),
+    (dict(x=A + 4), EALIGN), (dict(codes=B + 8), EALIGN), (dict(scale=CC + 2), EALIGN),
+    (dict(codes=A + 1024), EINVAL),                       # codes overlap the input
+    (dict(scale=B + 100 * 16), EINVAL),                   # scales overlap the codes
+    (dict(n=0), OK), (dict(n=0, x=None, codes=None, scale=None), OK),
+])
+def test_grad_quant_validation(kw, want):
+    assert gq(**kw) == want
+
+
+def enc(w_new=A, w_prev=B, dt=0, n=4096, group=128, codes=CC, scale=D, minv=D + 4096):
+    return sdp4.lib().sdp4_qwd_encode(w_new, w_prev, dt, n, group, codes, scale, minv, None)
+
+
+def dec(codes=A, scale=B, minv=B + 4096, n=4096, group=128, w=CC, dt=0):
+    return sdp4.lib().sdp4_qwd_decode(codes, scale, minv, n, group, w, dt, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dt=2), EINVAL), (dict(dt=-1), EINVAL), (dict(group=100), EINVAL), (dict(n=4000), EALIGN),
+    (dict(w_new=None), EINVAL), (dict(minv=None), EINVAL), (dict(w_prev=B + 2), EALIGN),
+    (dict(codes=CC + 4), EALIGN), (dict(minv=D + 1), EALIGN),
+    (dict(codes=A + 16), EINVAL), (dict(minv=D + 16), EINVAL), (dict(scale=B + 4 * 100), EINVAL),
+    (dict(n=0), OK),
+])
+def test_qwd_encode_validation(kw, want):
+    assert enc(**kw) == want
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dt=7), EINVAL), (dict(group=64 + 32), EINVAL), (dict(n=4096 + 64), EALIGN), (dict(w=None), EINVAL),
+    (dict(w=CC + 8), EALIGN), (dict(codes=A + 8), EALIGN), (dict(w=A + 512), EINVAL),
+    (dict(scale=CC + 100, w=CC), EINVAL), (dict(n=0), OK),
+])
+def test_qwd_decode_validation(kw, want):
+    assert dec(**kw) == want
+
+
+def dr(P=4, codes=None, scales=None, n=4096, bits_in=8, group=128, bits_out=4, block=0, out_scale=1.0,
+       oc=D, os_=D + (1 << 24), of=None, table_null=False):
+    if codes is None:
+        codes = [A + p * (1 << 20) for p in range(P)]
+    if scales is None:
+        scales = [B + p * (1 << 20) for p in range(P)]
+    cp = (C.c_void_p * max(len(codes), 1))(*codes)
+    sp = (C.c_void_p * max(len(scales), 1))(*scales)
+    ct = None if table_null else C.cast(cp, C.c_void_p)
+    st = None if table_null else C.cast(sp, C.c_void_p)
+    return sdp4.lib().sdp4_dequant_reduce(P, ct, st, n, bits_in, group, bits_out, block, out_scale, oc, os_,
+                                          of, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(P=0), ERANGE), (dict(P=17, codes=[A] * 17, scales=[B] * 17), ERANGE), (dict(P=-3), ERANGE),
+    (dict(bits_in=2), EINVAL), (dict(bits_out=2), EINVAL), (dict(bits_out=4, block=64), EINVAL),
+    (dict(out_scale=math.inf), EINVAL), (dict(out_scale=math.nan), EINVAL),
+    (dict(table_null=True), EINVAL), (dict(codes=[A, 0, A + 2 * (1 << 20), A + 3 * (1 << 20)]), EINVAL),
+    (dict(codes=[A, A + 8, A + 2 * (1 << 20), A + 3 * (1 << 20)]), EALIGN),
+    (dict(scales=[B, B + 2, B + 8, B + 12]), EALIGN),
+    (dict(oc=None), EINVAL), (dict(os_=None), EINVAL), (dict(bits_out=0, block=64, of=None), EINVAL),
+    (dict(n=4096 + 64), EALIGN), (dict(bits_out=0, block=256, n=128 * 3, of=D), EALIGN),
+    (dict(oc=A + 1024), EINVAL),                          # output codes overlap peer 0's codes
+    (dict(os_=B + 3 * (1 << 20) + 8), EINVAL),            # output scales overlap peer 3's scales
+    (dict(of=D + 256), EINVAL),                           # f32 output overlaps output codes
+    (dict(of=D + 8), EALIGN),
+    (dict(n=0), OK),
+])
+def test_dequant_reduce_validation(kw, want):
+    assert dr(**kw) == want
+
+
+def test_hadamard_reduce_copy_validation():
+    L = sdp4.lib()
+    assert L.sdp4_hadamard(A, B, 4096, 0, None) == EINVAL
+    assert L.sdp4_hadamard(A, B, 4096, 96, None) == EINVAL
+    assert L.sdp4_hadamard(A, B, 4000, 64, None) == EALIGN
+    assert L.sdp4_hadamard(A, A + 64, 4096, 64, None) == EINVAL      # partial overlap
+    assert L.sdp4_hadamard(A + 4, B, 4096, 64, None) == EALIGN
+    assert L.sdp4_hadamard(A, B, 0, 64, None) == OK
+    xs = (C.c_void_p * 2)(A, B)
+    assert L.sdp4_reduce_f32(0, C.cast(xs, C.c_void_p), CC, 1024, None) == ERANGE
+    assert L.sdp4_reduce_f32(17, C.cast(xs, C.c_void_p), CC, 1024, None) == ERANGE
+    assert L.sdp4_reduce_f32(2, C.cast(xs, C.c_void_p), A + 16, 1024, None) == EINVAL
+    assert L.sdp4_reduce_f32(2, C.cast(xs, C.c_void_p), CC + 4, 1024, None) == EALIGN
+    assert L.sdp4_reduce_f32(2, None, CC, 1024, None) == EINVAL
+    assert L.sdp4_copy_f32(A, A + 16, 1024, None) == EINVAL
+    assert L.sdp4_copy_f32(A, None, 1024, None) == EINVAL
+    assert L.sdp4_copy_f32(A, B, -1, None) == EINVAL
+    assert L.sdp4_copy_f32(A, B, 0, None) == OK
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(4096)
+    with pytest.raises(ValueError):
+        sdp4.sdp4_grad_quant(x, 8, 256, 128, x, x)

@@ -1,0 +1,427 @@
+"""GPU parity: every entry point of the HIP library against the oracle, on
+seeded inputs that span several wave tiles and end in a ragged tail, plus
+edge values, the two-level chain, and run-to-run determinism.
+
+All calls go through the C ABI (ctypes binding); the oracle sees the same
+host arrays the device received.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2410_15526_amd import sdp4
+from tests._chain import build_lattice_exact_peers, oracle_chain
+from tests._gpu import check_codes, check_f32, check_headers, dev, empty, host, say, torch
+
+pytestmark = pytest.mark.gpu
+
+TILE = 2048          # elements per wavefront tile of the kernels
+
+
+def size_for(lcm: int, target: int = 11000) -> int:
+    """A multiple of lcm near `target`: several tiles and, when lcm < TILE, a ragged tail."""
+    return lcm * max(1, -(-target // lcm))
+
+
+def sync():
+    torch().cuda.synchronize()
+
+
+def grad_input(n, seed=0, peer=None, kind="c3"):
+    w = synth.scaled(synth.WORKLOADS[kind], max(n, 1 << 20))
+    return synth.gradient(w, 0, n, seed=seed, peer=peer)
+
+
+# ----------------------------------------------------------------------------
+# K1: Hadamard + group quantization
+# ----------------------------------------------------------------------------
+
+def run_grad_quant(x: np.ndarray, bits, block, group):
+    n = x.size
+    xd = dev(x)
+    codes = empty(n * bits // 8, "u8")
+    scale = empty(n // group, "f32")
+    sdp4.sdp4_grad_quant(xd, bits, block, group, codes, scale)
+    sync()
+    return host(codes), host(scale)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("block", [0, 2, 4, 16, 32, 64, 128, 256, 512, 1024])
+@pytest.mark.parametrize("group", [32, 64, 128, 256, 512, 2048, 4096])
+def test_grad_quant(bits, block, group):
+    n = size_for(max(group, block))
+    say(f"grad_quant bits={bits} block={block} group={group} n={n}")
+    x = grad_input(n, seed=bits * 1000 + block + group)
+    codes, scale = run_grad_quant(x, bits, block, group)
+    rc, rs, pre = oracle.grad_quant(x, bits, block, group)
+    check_headers(scale, rs)
+    check_codes(codes, rc, pre, n, bits)
+
+
+def edge_gradient(n):
+    r = np.random.default_rng(7)
+    x = (r.standard_normal(n) * 1e-3).astype(np.float32)
+    g = 128
+    x[0:g] = 0.0                                     # zero group
+    x[g:2 * g] = -0.0
+    x[2 * g:3 * g] = 0.3                             # constant group
+    x[3 * g:4 * g] = (r.standard_normal(g) * 1e-41).astype(np.float32)   # denormals
+    x[4 * g:5 * g] = (r.standard_normal(g) * 1e37).astype(np.float32)    # huge
+    x[5 * g:6 * g] = 0.0
+    x[5 * g + 17] = -2.5                             # single outlier in a zero group
+    x[6 * g:7 * g] = np.float32(1e-37)               # tiny normal: qmax / s still finite
+    x[7 * g:8 * g] = r.choice(np.float32([-1, 1]), g) * np.float32(2.0 ** -20)
+    x[8 * g:9 * g] = np.linspace(-127, 127, g).astype(np.float32)         # exact lattice
+    x[9 * g:10 * g] = (np.arange(g) - 63.5).astype(np.float32) / 127      # ties at k + 1/2
+    return x
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("block", [0, 128, 256])
+def test_grad_quant_edge_values(bits, block):
+    n = size_for(256, 4096)
+    say(f"grad_quant edge bits={bits} block={block}")
+    x = edge_gradient(n)
+    codes, scale = run_grad_quant(x, bits, block, 128)
+    rc, rs, pre = oracle.grad_quant(x, bits, block, 128)
+    check_headers(scale, rs)
+    check_codes(codes, rc, pre, n, bits)
+
+
+# ----------------------------------------------------------------------------
+# qWD encode / decode
+# ----------------------------------------------------------------------------
+
+def qwd_inputs(n, prev_dtype, seed=0):
+    w = synth.scaled(synth.WORKLOADS["c4" if prev_dtype == "bf16" else "c2"], max(n, 1 << 20))
+    prev = synth.prev_weights(w, 0, n, seed=seed)
+    new = synth.new_weights(w, 0, n, seed=seed)
+    return new, prev
+
+
+def run_qwd(new, prev, group):
+    n = new.size
+    nd, pd = dev(new), dev(prev)
+    codes, scale, minv = empty(n // 2, "u8"), empty(n // group, "f32"), empty(n // group, "f32")
+    sdp4.sdp4_qwd_encode(nd, pd, group, codes, scale, minv)
+    sdp4.sdp4_qwd_decode(codes, scale, minv, group, pd)
+    sync()
+    return host(codes), host(scale), host(minv), host(pd)
+
+
+@pytest.mark.parametrize("prev_dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("group", [32, 64, 128, 256, 1024, 2048, 4096])
+def test_qwd_encode_decode(prev_dtype, group):
+    n = size_for(group)
+    say(f"qwd prev={prev_dtype} group={group} n={n}")
+    new, prev = qwd_inputs(n, prev_dtype, seed=group)
+    codes, scale, minv, upd = run_qwd(new, prev, group)
+    rc, rs, rm, pre = oracle.qwd_encode(new, prev, group)
+    check_headers(minv, rm, "minv")
+    check_headers(scale, rs)
+    check_codes(codes, rc, pre, n, 4, signed=False)
+    want = oracle.qwd_decode(rc, rs, rm, prev, group)
+    if prev_dtype == "bf16":
+        assert np.array_equal(upd, want)
+    else:
+        check_f32(upd, want, "updated weights")
+
+
+def test_qwd_decode_stage_isolated():
+    """Decode of the oracle's own message (not the GPU encoder's)."""
+    n, group = size_for(128), 128
+    for prev_dtype in ("f32", "bf16"):
+        say(f"qwd decode isolated prev={prev_dtype}")
+        new, prev = qwd_inputs(n, prev_dtype, seed=3)
+        rc, rs, rm, _ = oracle.qwd_encode(new, prev, group)
+        pd = dev(prev)
+        sdp4.sdp4_qwd_decode(dev(rc), dev(rs), dev(rm), group, pd)
+        sync()
+        want = oracle.qwd_decode(rc, rs, rm, prev, group)
+        got = host(pd)
+        if prev_dtype == "bf16":
+            assert np.array_equal(got, want)
+        else:
+            check_f32(got, want)
+
+
+@pytest.mark.parametrize("prev_dtype", ["f32", "bf16"])
+def test_qwd_edge_values(prev_dtype):
+    n, g = size_for(128, 4096), 128
+    say(f"qwd edge prev={prev_dtype}")
+    new, prev = qwd_inputs(n, prev_dtype, seed=9)
+    base = synth.bf16_bits_to_f32(prev) if prev_dtype == "bf16" else prev
+    new = new.copy()
+    new[0:g] = base[0:g]                                  # zero difference
+    new[g:2 * g] = base[g:2 * g] + np.float32(1e-3)       # (nearly) constant difference
+    new[2 * g:3 * g] = base[2 * g:3 * g] + np.float32(1e30) * np.sign(np.arange(g) - 60)
+    new[3 * g:4 * g] = base[3 * g:4 * g] + np.float32(1e-42)
+    new[4 * g] = base[4 * g] + np.float32(5.0)            # one large update in a group
+    codes, scale, minv, upd = run_qwd(new, prev, g)
+    rc, rs, rm, pre = oracle.qwd_encode(new, prev, g)
+    check_headers(minv, rm, "minv")
+    check_headers(scale, rs)
+    check_codes(codes, rc, pre, n, 4, signed=False)
+    want = oracle.qwd_decode(rc, rs, rm, prev, g)
+    if prev_dtype == "bf16":
+        assert np.array_equal(upd, want)
+    else:
+        check_f32(upd, want)
+
+
+def test_qw_variant_is_encode_from_zero():
+    """qW (direct 4-bit weight quantization, Sec. 5.1 baseline) = qWD against zero weights."""
+    n, g = size_for(2048), 2048
+    say("qW variant")
+    w = synth.prev_weights(synth.scaled(synth.WORKLOADS["c2"], 1 << 20), 0, n)
+    zero = np.zeros(n, np.float32)
+    codes, scale, minv, upd = run_qwd(w, zero, g)
+    rc, rs, rm, pre = oracle.qwd_encode(w, zero, g)
+    check_codes(codes, rc, pre, n, 4, signed=False)
+    check_headers(scale, rs)
+    check_f32(upd, oracle.qwd_decode(rc, rs, rm, zero, g))
+
+
+# ----------------------------------------------------------------------------
+# K2 / K3: dequantize + reduce
+# ----------------------------------------------------------------------------
+
+def peer_messages(P, n, bits, block, group, seed=0):
+    """Oracle-made messages of P synthetic peers (stage-isolated inputs)."""
+    out = []
+    for p in range(P):
+        x = grad_input(n, seed=seed, peer=p)
+        c, s, _ = oracle.grad_quant(x, bits, block, group)
+        out.append((c, s))
+    return out
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 4, 5, 8, 16])
+@pytest.mark.parametrize("bits_in,bits_out", [(8, 4), (8, 8), (4, 4), (4, 8)])
+@pytest.mark.parametrize("group", [32, 128, 4096])
+def test_dequant_reduce_requant(P, bits_in, bits_out, group):
+    n = size_for(group)
+    say(f"dequant_reduce requant P={P} in={bits_in} out={bits_out} group={group} n={n}")
+    msgs = peer_messages(P, n, bits_in, 256 if group >= 256 else 0, group, seed=P)
+    cd = [dev(c) for c, _ in msgs]
+    sd = [dev(s) for _, s in msgs]
+    oc, os_, of = empty(n * bits_out // 8, "u8"), empty(n // group, "f32"), empty(n, "f32")
+    sdp4.sdp4_dequant_reduce(cd, sd, n, bits_in, group, bits_out, 0, 1.0, oc, os_, of)
+    oc2, os2 = empty(n * bits_out // 8, "u8"), empty(n // group, "f32")
+    sdp4.sdp4_dequant_reduce(cd, sd, n, bits_in, group, bits_out, 0, 1.0, oc2, os2, None)
+    sync()
+    ref = oracle.dequant_reduce([c for c, _ in msgs], [s for _, s in msgs], n, bits_in, group, bits_out)
+    check_f32(host(of), ref["f32"], "reduced")
+    check_headers(host(os_), ref["scales"])
+    check_codes(host(oc), ref["codes"], ref["pre"], n, bits_out)
+    assert np.array_equal(host(oc2), host(oc)) and np.array_equal(host(os2), host(os_))
+
+
+@pytest.mark.parametrize("P", [1, 2, 4, 7, 16])
+@pytest.mark.parametrize("bits_in", [4, 8])
+@pytest.mark.parametrize("block", [0, 2, 64, 128, 256, 1024])
+@pytest.mark.parametrize("out_scale", [1.0, 0.125, 1.0 / 3.0])
+def test_dequant_reduce_to_f32(P, bits_in, block, out_scale):
+    group = 128
+    n = size_for(max(group, block))
+    say(f"dequant_reduce f32 P={P} in={bits_in} block={block} out_scale={out_scale} n={n}")
+    msgs = peer_messages(P, n, bits_in, 0, group, seed=10 + P)
+    of = empty(n, "f32")
+    sdp4.sdp4_dequant_reduce([dev(c) for c, _ in msgs], [dev(s) for _, s in msgs], n, bits_in, group, 0,
+                             block, out_scale, None, None, of)
+    sync()
+    ref = oracle.dequant_reduce([c for c, _ in msgs], [s for _, s in msgs], n, bits_in, group, 0, block,
+                                out_scale)
+    check_f32(host(of), ref["f32"])
+
+
+def test_dequant_reduce_wide_group_to_f32():
+    n, group = 3 * 4096, 4096
+    say("dequant_reduce f32 group 4096")
+    msgs = peer_messages(3, n, 4, 0, group, seed=77)
+    of = empty(n, "f32")
+    sdp4.sdp4_dequant_reduce([dev(c) for c, _ in msgs], [dev(s) for _, s in msgs], n, 4, group, 0, 1024,
+                             0.5, None, None, of)
+    sync()
+    ref = oracle.dequant_reduce([c for c, _ in msgs], [s for _, s in msgs], n, 4, group, 0, 1024, 0.5)
+    check_f32(host(of), ref["f32"])
+
+
+# ----------------------------------------------------------------------------
+# standalone pieces of the unfused variant
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("block", [2, 8, 32, 64, 128, 256, 512, 1024])
+def test_hadamard(block):
+    n = size_for(block)
+    say(f"hadamard block={block} n={n}")
+    x = grad_input(n, seed=block)
+    xd = dev(x)
+    y = empty(n, "f32")
+    sdp4.sdp4_hadamard(xd, y, block)
+    sdp4.sdp4_hadamard(xd, xd, block)          # in place
+    sync()
+    want = oracle.hadamard(x, block)
+    check_f32(host(y), want)
+    check_f32(host(xd), want, "in place")
+
+
+@pytest.mark.parametrize("P", [1, 2, 5, 16])
+@pytest.mark.parametrize("n", [4096, 4099, 1 << 20])
+def test_reduce_f32_and_copy(P, n):
+    say(f"reduce_f32 P={P} n={n}")
+    r = np.random.default_rng(P)
+    xs = [(r.standard_normal(n) * 10.0 ** r.uniform(-3, 3)).astype(np.float32) for _ in range(P)]
+    y = empty(n, "f32")
+    sdp4.sdp4_reduce_f32([dev(x) for x in xs], y)
+    z = empty(n, "f32")
+    x0 = dev(xs[0])
+    sdp4.sdp4_copy_f32(x0, z)
+    sync()
+    check_f32(host(y), oracle.reduce_f32(xs))
+    assert np.array_equal(host(z), xs[0])
+
+
+# ----------------------------------------------------------------------------
+# the two-level chain, run the way one GPU runs it
+# ----------------------------------------------------------------------------
+
+def gpu_chain(grads, P, Q, group, block, out_scale=1.0):
+    """K1 per peer, K2 per node (pointer slices as the all-to-all would deliver), K3."""
+    M = grads[0][0].size
+    m = M // Q
+    level2 = []
+    for a in range(Q):
+        codes, scales = [], []
+        for b in range(P):
+            c, s = empty(M, "u8"), empty(M // group, "f32")
+            sdp4.sdp4_grad_quant(dev(grads[a][b]), 8, block, group, c, s)
+            codes.append(c)
+            scales.append(s)
+        oc, os_ = empty(M // 2, "u8"), empty(M // group, "f32")
+        sdp4.sdp4_dequant_reduce(codes, scales, M, 8, group, 4, 0, 1.0, oc, os_)
+        level2.append((oc, os_))
+    out = empty(m, "f32")
+    sdp4.sdp4_dequant_reduce([oc[:m // 2] for oc, _ in level2], [os_[:m // group] for _, os_ in level2], m, 4,
+                             group, 0, block, out_scale, None, None, out)
+    sync()
+    return host(out)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_chain_matches_oracle(name):
+    w = synth.WORKLOADS[name]
+    P, Q, group, block = w.P, w.Q, w.group, w.hadamard_block
+    M = Q * size_for(max(group, block), 4096)
+    say(f"chain {name} P={P} Q={Q} block={block} M={M}")
+    ws = synth.scaled(w, 1 << 20)
+    grads = [[synth.gradient(ws, 0, M, seed=5, peer=a * P + b) for b in range(P)] for a in range(Q)]
+    got = gpu_chain(grads, P, Q, group, block, out_scale=1.0 / (P * Q))
+    want = oracle_chain(grads, P, Q, group, block, out_scale=1.0 / (P * Q))
+    check_f32(got, want)
+
+
+@pytest.mark.parametrize("block", [0, 16, 64, 256])
+def test_chain_lattice_exact_is_reduce_scatter(block):
+    P, Q, group = 8, 4, 128
+    say(f"lattice chain block={block}")
+    grads, want = build_lattice_exact_peers(P, Q, group=group, block=block, m_out=2048, seed=block + 1)
+    got = gpu_chain(grads, P, Q, group, block)
+    assert np.array_equal(got.astype(np.float64), want)
+
+
+def test_unfused_chain_matches_oracle():
+    """The 'HS w/o fused' variant: standalone transform, plain (de)quantization
+    per chunk, float32 reductions, standalone inverse transform."""
+    P, Q, group, block = 4, 2, 128, 256
+    M = Q * size_for(256, 4096)
+    m = M // Q
+    say("unfused chain")
+    ws = synth.scaled(synth.WORKLOADS["c3"], 1 << 20)
+    grads = [[synth.gradient(ws, 0, M, seed=6, peer=a * P + b) for b in range(P)] for a in range(Q)]
+    level2_dev, level2_ref = [], []
+    for a in range(Q):
+        deq_dev, deq_ref = [], []
+        for b in range(P):
+            xd = dev(grads[a][b])
+            hd = empty(M, "f32")
+            sdp4.sdp4_hadamard(xd, hd, block)
+            c, s = empty(M, "u8"), empty(M // group, "f32")
+            sdp4.sdp4_grad_quant(hd, 8, 0, group, c, s)
+            f = empty(M, "f32")
+            sdp4.sdp4_dequant_reduce([c], [s], M, 8, group, 0, 0, 1.0, None, None, f)
+            deq_dev.append(f)
+            rc, rs, _ = oracle.grad_quant(oracle.hadamard(grads[a][b], block), 8, 0, group)
+            deq_ref.append(oracle.dequant_reduce([rc], [rs], M, 8, group, 0)["f32"])
+        red = empty(M, "f32")
+        sdp4.sdp4_reduce_f32(deq_dev, red)
+        c4, s4 = empty(M // 2, "u8"), empty(M // group, "f32")
+        sdp4.sdp4_grad_quant(red, 4, 0, group, c4, s4)
+        level2_dev.append((c4, s4))
+        rc4, rs4, _ = oracle.grad_quant(oracle.reduce_f32(deq_ref), 4, 0, group)
+        level2_ref.append((rc4, rs4))
+    parts_dev, parts_ref = [], []
+    for (c4, s4), (rc4, rs4) in zip(level2_dev, level2_ref):
+        f = empty(m, "f32")
+        sdp4.sdp4_dequant_reduce([c4[:m // 2]], [s4[:m // group]], m, 4, group, 0, 0, 1.0, None, None, f)
+        parts_dev.append(f)
+        parts_ref.append(oracle.dequant_reduce([rc4[:m // 2]], [rs4[:m // group]], m, 4, group, 0)["f32"])
+    red = empty(m, "f32")
+    sdp4.sdp4_reduce_f32(parts_dev, red)
+    out = empty(m, "f32")
+    sdp4.sdp4_hadamard(red, out, block)
+    sync()
+    want = oracle.hadamard(oracle.reduce_f32(parts_ref), block)
+    check_f32(host(out), want)
+
+
+# ----------------------------------------------------------------------------
+# determinism, empty inputs, binding errors
+# ----------------------------------------------------------------------------
+
+def test_bitwise_repeatable():
+    n, group, block = 1 << 21, 128, 256
+    say("repeatability")
+    x = dev(grad_input(n, seed=3))
+    outs = []
+    for _ in range(3):
+        c, s = empty(n, "u8"), empty(n // group, "f32")
+        sdp4.sdp4_grad_quant(x, 8, block, group, c, s)
+        oc, os_ = empty(n // 8, "u8"), empty(n // 4 // group, "f32")
+        sdp4.sdp4_dequant_reduce([c[i * n // 4:(i + 1) * n // 4] for i in range(4)],
+                                 [s[i * n // 4 // group:(i + 1) * n // 4 // group] for i in range(4)],
+                                 n // 4, 8, group, 4, 0, 1.0, oc, os_)
+        f = empty(n // 16, "f32")
+        sdp4.sdp4_dequant_reduce([oc[i * n // 32:(i + 1) * n // 32] for i in range(2)],
+                                 [os_[i * n // 16 // group:(i + 1) * n // 16 // group] for i in range(2)],
+                                 n // 16, 4, group, 0, block, 0.125, None, None, f)
+        sync()
+        outs.append((host(c), host(s), host(oc), host(os_), host(f)))
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+def test_empty_inputs_are_noops():
+    say("empty inputs")
+    z = empty(16, "f32")
+    sentinel = z.clone()
+    sdp4.sdp4_grad_quant(z, 8, 256, 128, z[:0], z[:0], n=0)
+    sdp4.sdp4_hadamard(z, z, 64, n=0)
+    sdp4.sdp4_dequant_reduce([z], [z], 0, 8, 128, 0, 0, 1.0, None, None, z)
+    sync()
+    assert torch().equal(z, sentinel)
+
+
+def test_binding_reports_status():
+    say("binding errors")
+    x = empty(4096 + 4, "f32")
+    c, s = empty(4096, "u8"), empty(32, "f32")
+    with pytest.raises(sdp4.Sdp4Error) as e:
+        sdp4.sdp4_grad_quant(x[1:4097], 8, 256, 128, c, s)          # 4-byte offset: misaligned
+    assert e.value.status == sdp4.EALIGN
+    with pytest.raises(sdp4.Sdp4Error) as e:
+        sdp4.sdp4_grad_quant(x[:4096], 8, 256, 96, c, s)
+    assert e.value.status == sdp4.EINVAL
