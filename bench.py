@@ -1,0 +1,237 @@
+"""Benchmark of one GPU's share of the SDP4Bit hot path on MI355X.
+
+A step is one pass of the whole path over the GPT-13B 1/8 shard
+(N = 1,625,292,800 elements; bf16 model weights, qWD group 128; Hadamard
+block 256, group 128, 8-bit x P=8 then 4-bit x Q=4): qWD encode, qWD
+decode, Hadamard + 8-bit quantization, 8-bit dequantize-reduce with 4-bit
+re-quantization, 4-bit dequantize-reduce with the inverse Hadamard.  Inputs
+are seeded synthetic data resident in HBM before timing starts.
+
+Prints one JSON line.  ``value`` is the fp32-equivalent input throughput of
+the step: 4 bytes x (input elements of every kernel) / step time.  Per
+kernel the line also carries algorithmic HBM bytes / launch time against the
+8 TB/s HBM peak; ``roofline`` is that figure for the kernel that takes the
+largest share of the step.  ``cpu_baseline`` is the plain CPU oracle timed
+on a bounded sample of the same workload on this host (single thread).
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload c5]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "GB/s of fp32 input processed per kernel (quant, dequant-reduce); % of HBM peak"
+SLAB = 1 << 26
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def fill(dst, gen, n):
+    """Generate host data slab by slab and copy it into the device tensor."""
+    import numpy as np
+    import torch
+    for s in range(0, n, SLAB):
+        k = min(SLAB, n - s)
+        a = np.ascontiguousarray(gen(s, k))
+        t = torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a)
+        if a.dtype == np.uint16:
+            dst[s:s + k].view(torch.int16).copy_(t)
+        else:
+            dst[s:s + k].copy_(t)
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2410_15526_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel: str):
+    """HBM traffic per launch from the committed rocprofv3 counter summary,
+    or None when that summary is missing or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except ValueError:
+        return None
+    if d.get("source_digest") != source_digest():
+        return None
+    k = d.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("bytes_per_launch")
+
+
+def cpu_baseline(w, sample_log2: int, seed: int):
+    """The oracle on a contiguous sample of the workload: one full step."""
+    import numpy as np
+    import oracle
+    import synth
+    n = 1 << sample_log2
+    P, Q, g, hb, qg = w.P, w.Q, w.group, w.hadamard_block, w.qwd_group
+    prev = synth.prev_weights(w, 0, n, seed)
+    new = synth.new_weights(w, 0, n, seed)
+    grad = synth.gradient(w, 0, n, seed)
+    M, m = n // P, n // P // Q
+    t0 = time.perf_counter()
+    c, s, mn, _ = oracle.qwd_encode(new, prev, qg)
+    oracle.qwd_decode(c, s, mn, prev, qg)
+    k1c, k1s, _ = oracle.grad_quant(grad, 8, hb, g)
+    r = oracle.dequant_reduce([k1c[p * M:(p + 1) * M] for p in range(P)],
+                              [k1s[p * M // g:(p + 1) * M // g] for p in range(P)], M, 8, g, 4, want_f32=False)
+    oracle.dequant_reduce([r["codes"][q * m // 2:(q + 1) * m // 2] for q in range(Q)],
+                          [r["scales"][q * m // g:(q + 1) * m // g] for q in range(Q)], m, 4, g, 0, hb,
+                          1.0 / (P * Q))
+    dt = time.perf_counter() - t0
+    fp32_bytes = 4 * (n + n + n + n + n // P)
+    return {"value": round(fp32_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "seconds": round(dt, 3),
+            "sample": f"elements [0, 2^{sample_log2}) of the same workload, one full step "
+                      f"(qWD encode+decode, Hadamard+8-bit, 8-bit x{P} reduce + 4-bit, 4-bit x{Q} reduce + "
+                      f"inverse Hadamard), single-threaded plain C oracle"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c5")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-sample-log2", type=int, default=29)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU's share of the hot path; runs on more than one GPU are not "
+              "supported by this build (the collectives between the kernels are out of scope).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_2410_15526_amd import sdp4
+    from paper_2410_15526_amd.pipeline import HotPath
+
+    w = synth.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    hp = HotPath(w.n, w.group, w.hadamard_block, w.P, w.Q, w.qwd_group, w.prev_dtype)
+    t_fill = time.perf_counter()
+    fill(hp.w_prev, lambda s, k: synth.prev_weights(w, s, k, args.seed), w.n)
+    fill(hp.w_new, lambda s, k: synth.new_weights(w, s, k, args.seed), w.n)
+    fill(hp.grad, lambda s, k: synth.gradient(w, s, k, args.seed), w.n)
+    torch.cuda.synchronize()
+    log(f"inputs ready in {time.perf_counter() - t_fill:.1f} s: {w.describe()}")
+
+    # copy-kernel yardstick (2 GiB read + 2 GiB written)
+    cn = 1 << 29
+    src = torch.empty(cn, device="cuda")
+    dst = torch.empty(cn, device="cuda")
+    for _ in range(3):
+        sdp4.sdp4_copy_f32(src, dst)
+    torch.cuda.synchronize()
+    ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ce[0].record()
+    for _ in range(10):
+        sdp4.sdp4_copy_f32(src, dst)
+    ce[1].record()
+    torch.cuda.synchronize()
+    copy_gbps = 2 * 4 * cn * 10 / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
+    del src, dst
+
+    for _ in range(args.warmup):
+        hp.step()
+    torch.cuda.synchronize()
+    events = {}
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        hp.step(events=events)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
+
+    info = hp.kernel_info()
+    kernels = {}
+    for name, pairs in events.items():
+        ms = sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
+        ki = info[name]
+        alg = ki.alg_bytes / (ms * 1e-3) / 1e9
+        kernels[name] = {"ms": round(ms, 4), "alg_bytes": ki.alg_bytes, "alg_GBps": round(alg, 1),
+                         "hbm_frac": round(alg / HBM_PEAK_GBPS, 4),
+                         "fp32_in_GBps": round(ki.fp32_in_bytes / (ms * 1e-3) / 1e9, 1),
+                         "elems_per_s": round(ki.fp32_in_bytes / 4 / (ms * 1e-3), 1)}
+    dom = max(kernels, key=lambda k: kernels[k]["ms"])
+    dk = kernels[dom]
+    fp32_total = sum(k.fp32_in_bytes for k in info.values())
+    value = fp32_total / (ms_step * 1e-3) / 1e9
+
+    unfused = None
+    if not args.no_unfused:
+        for _ in range(2):
+            hp.unfused_gradient_step()
+        torch.cuda.synchronize()
+        ue = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ue[0].record()
+        for _ in range(5):
+            hp.grad_quant(); hp.reduce_intra(); hp.reduce_inter()
+        ue[1].record()
+        ue[2].record()
+        for _ in range(5):
+            hp.unfused_gradient_step()
+        ue[3].record()
+        torch.cuda.synchronize()
+        unfused = {"fused_gradient_ms": round(ue[0].elapsed_time(ue[1]) / 5, 4),
+                   "unfused_gradient_ms": round(ue[2].elapsed_time(ue[3]) / 5, 4)}
+
+    traffic = traffic_for(dom)
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.describe(), "n": w.n, "hadamard_block": w.hadamard_block,
+                   "group": w.group, "P": w.P, "Q": w.Q, "qwd_group": w.qwd_group,
+                   "model_weights": w.prev_dtype, "gradient_bits": [8, 4]},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": dk["alg_GBps"], "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(dk["alg_GBps"] / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic},
+        "kernels": kernels,
+        "copy_GBps": round(copy_gbps, 1),
+        "step_alg_GBps": round(sum(k.alg_bytes for k in info.values()) / (ms_step * 1e-3) / 1e9, 1),
+    }
+    if unfused:
+        line["hadamard_fusion"] = unfused
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample ...")
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_log2, args.seed)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

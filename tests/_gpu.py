@@ -96,3 +96,15 @@ def check_f32(got, want, what: str = "f32", exact: bool = True):
     if exact:
         bad = np.nonzero(got.view(np.uint32) != want.view(np.uint32))[0]
         assert bad.size == 0, (what, "not bit-exact", bad[:10], got[bad[:10]], want[bad[:10]])
+
+
+def fill(dst, gen, n, slab=1 << 26):
+    """Generate host data slab by slab (gen(start, count)) and copy it into a device tensor."""
+    t = torch()
+    for s in range(0, n, slab):
+        k = min(slab, n - s)
+        a = np.ascontiguousarray(gen(s, k))
+        if a.dtype == np.uint16:
+            dst[s:s + k].view(t.int16).copy_(t.from_numpy(a.view(np.int16)))
+        else:
+            dst[s:s + k].copy_(t.from_numpy(a))

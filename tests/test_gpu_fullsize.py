@@ -1,0 +1,169 @@
+"""Parity at the full shard sizes of the five workloads, in the launch
+configuration the benchmark times (paper_2410_15526_amd.pipeline.HotPath).
+
+The GPU runs one full step on the whole shard.  The oracle then recomputes
+sampled segments from regenerated inputs (the generators are addressable by
+element range), following the same chunk routing: an output segment of the
+final 4-bit reduction needs the matching segment of each of the Q 4-bit
+chunks, each of which needs the matching segment of each of the P 8-bit
+chunks.  Segments include the first and the last of every buffer (the
+ragged end of the last wave tile) and random ones in between.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2410_15526_amd import sdp4
+from paper_2410_15526_amd.pipeline import HotPath
+from tests._gpu import check_codes, check_f32, check_headers, fill, host, say, torch
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def segments(length, seg, count, seed):
+    """Start offsets (multiples of seg) of `count` segments inside [0, length)."""
+    r = np.random.default_rng(seed)
+    k = length // seg
+    picks = {0, k - 1} | set(int(v) for v in r.integers(0, k, count))
+    return sorted(p * seg for p in picks)
+
+
+def build(w, seed=0):
+    hp = HotPath(w.n, w.group, w.hadamard_block, w.P, w.Q, w.qwd_group, w.prev_dtype)
+    say(f"fill {w.describe()}")
+    fill(hp.w_prev, lambda s, k: synth.prev_weights(w, s, k, seed), w.n)
+    fill(hp.w_new, lambda s, k: synth.new_weights(w, s, k, seed), w.n)
+    fill(hp.grad, lambda s, k: synth.gradient(w, s, k, seed), w.n)
+    torch().cuda.synchronize()
+    return hp
+
+
+def check_qwd(hp, w, seed, starts, L):
+    g = w.qwd_group
+    for a in starts:
+        new = synth.new_weights(w, a, L, seed)
+        prev = synth.prev_weights(w, a, L, seed)
+        rc, rs, rm, pre = oracle.qwd_encode(new, prev, g)
+        check_codes(host(hp.qcodes[a // 2:(a + L) // 2]), rc, pre, L, 4, signed=False, what=f"qwd@{a}")
+        check_headers(host(hp.qscale[a // g:(a + L) // g]), rs, f"qscale@{a}")
+        check_headers(host(hp.qmin[a // g:(a + L) // g]), rm, f"qmin@{a}")
+        want = oracle.qwd_decode(rc, rs, rm, prev, g)
+        got = host(hp.w_prev[a:a + L])
+        assert np.array_equal(got.view(np.uint8), np.ascontiguousarray(want).view(np.uint8)), f"decode@{a}"
+
+
+def k1_ref(w, seed, a, L):
+    x = synth.gradient(w, a, L, seed)
+    return oracle.grad_quant(x, 8, w.hadamard_block, w.group)
+
+
+def k2_ref(w, seed, x, L):
+    """Oracle K2 output segment [x, x+L) of the intra-node reduction."""
+    M, g = w.n // w.P, w.group
+    k1 = [k1_ref(w, seed, p * M + x, L) for p in range(w.P)]
+    return oracle.dequant_reduce([c for c, _, _ in k1], [s for _, s, _ in k1], L, 8, g, 4, want_f32=False)
+
+
+def check_gradient_path(hp, w, seed, starts_k1, starts_k3, L):
+    g, M, m = w.group, w.n // w.P, w.n // w.P // w.Q
+    for a in starts_k1:
+        rc, rs, pre = k1_ref(w, seed, a, L)
+        check_codes(host(hp.c8[a:a + L]), rc, pre, L, 8, what=f"k1@{a}")
+        check_headers(host(hp.s8[a // g:(a + L) // g]), rs, f"k1 scale@{a}")
+    for a in starts_k3:
+        parts = []
+        for q in range(w.Q):
+            r = k2_ref(w, seed, q * m + a, L)
+            x = q * m + a
+            check_codes(host(hp.c4[x // 2:(x + L) // 2]), r["codes"], r["pre"], L, 4, what=f"k2@{x}")
+            check_headers(host(hp.s4[x // g:(x + L) // g]), r["scales"], f"k2 scale@{x}")
+            parts.append(r)
+        want = oracle.dequant_reduce([r["codes"] for r in parts], [r["scales"] for r in parts], L, 4, g, 0,
+                                     w.hadamard_block, 1.0 / (w.P * w.Q))["f32"]
+        check_f32(host(hp.out[a:a + L]), want, f"k3@{a}")
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+def test_full_shard_step(name):
+    w = synth.WORKLOADS[name]
+    seed = 0
+    hp = build(w, seed)
+    say(f"{name}: one step of the hot path on N={w.n:,}")
+    hp.step()
+    torch().cuda.synchronize()
+    L = 4 * max(w.group, w.hadamard_block, w.qwd_group)
+    m = w.n // w.P // w.Q
+    check_qwd(hp, w, seed, segments(w.n, L, 12, 1), L)
+    check_gradient_path(hp, w, seed, segments(w.n, L, 12, 2), segments(m, L, 6, 3), L)
+    say(f"{name}: sampled parity ok")
+
+    if name == "c4":
+        # group-size sweep of the gradient quantizer and of qWD at the full size
+        for g in (32, 64, 256, 512):
+            say(f"c4 grad_quant group {g}")
+            c8 = torch().empty(w.n, dtype=torch().uint8, device="cuda")
+            s8 = torch().empty(w.n // g, device="cuda")
+            sdp4.sdp4_grad_quant(hp.grad, 8, w.hadamard_block, g, c8, s8)
+            torch().cuda.synchronize()
+            for a in segments(w.n, 4 * max(g, w.hadamard_block), 8, g):
+                Lg = 4 * max(g, w.hadamard_block)
+                rc, rs, pre = oracle.grad_quant(synth.gradient(w, a, Lg, seed), 8, w.hadamard_block, g)
+                check_codes(host(c8[a:a + Lg]), rc, pre, Lg, 8, what=f"k1 g{g}@{a}")
+                check_headers(host(s8[a // g:(a + Lg) // g]), rs)
+            del c8, s8
+        for qg in (64, 256):
+            say(f"c4 qWD group {qg}")
+            codes = torch().empty(w.n // 2, dtype=torch().uint8, device="cuda")
+            sc = torch().empty(w.n // qg, device="cuda")
+            mn = torch().empty(w.n // qg, device="cuda")
+            fill(hp.w_prev, lambda s, k: synth.prev_weights(w, s, k, seed), w.n)
+            sdp4.sdp4_qwd_encode(hp.w_new, hp.w_prev, qg, codes, sc, mn)
+            torch().cuda.synchronize()
+            for a in segments(w.n, 4 * qg, 8, qg):
+                Lq = 4 * qg
+                rc, rs, rm, pre = oracle.qwd_encode(synth.new_weights(w, a, Lq, seed),
+                                                    synth.prev_weights(w, a, Lq, seed), qg)
+                check_codes(host(codes[a // 2:(a + Lq) // 2]), rc, pre, Lq, 4, signed=False)
+                check_headers(host(sc[a // qg:(a + Lq) // qg]), rs)
+                check_headers(host(mn[a // qg:(a + Lq) // qg]), rm)
+    if name == "c5":
+        # the float32 model-weight variant of qWD at the full size
+        say("c5 qWD with float32 model weights")
+        prev32 = torch().empty(w.n, device="cuda")
+        fill(prev32, lambda s, k: synth.bf16_bits_to_f32(synth.prev_weights(w, s, k, seed)), w.n)
+        sdp4.sdp4_qwd_encode(hp.w_new, prev32, w.qwd_group, hp.qcodes, hp.qscale, hp.qmin)
+        sdp4.sdp4_qwd_decode(hp.qcodes, hp.qscale, hp.qmin, w.qwd_group, prev32)
+        torch().cuda.synchronize()
+        g = w.qwd_group
+        for a in segments(w.n, 4 * g, 8, 11):
+            Lq = 4 * g
+            prev = synth.bf16_bits_to_f32(synth.prev_weights(w, a, Lq, seed))
+            rc, rs, rm, pre = oracle.qwd_encode(synth.new_weights(w, a, Lq, seed), prev, g)
+            check_codes(host(hp.qcodes[a // 2:(a + Lq) // 2]), rc, pre, Lq, 4, signed=False)
+            check_f32(host(prev32[a:a + Lq]), oracle.qwd_decode(rc, rs, rm, prev, g))
+
+
+def test_tiny_shard_step_every_element():
+    """c1 at its full size, every output element of the step compared."""
+    w = synth.WORKLOADS["c1"]
+    hp = build(w, 0)
+    say("c1: one step, full comparison")
+    hp.step()
+    torch().cuda.synchronize()
+    n, g, P, Q, M, m = w.n, w.group, w.P, w.Q, w.n // w.P, w.n // w.P // w.Q
+    new, prev = synth.new_weights(w, 0, n), synth.prev_weights(w, 0, n)
+    rc, rs, rm, pre = oracle.qwd_encode(new, prev, w.qwd_group)
+    check_codes(host(hp.qcodes), rc, pre, n, 4, signed=False)
+    check_f32(host(hp.w_prev), oracle.qwd_decode(rc, rs, rm, prev, w.qwd_group))
+    k1c, k1s, pre1 = oracle.grad_quant(synth.gradient(w, 0, n), 8, w.hadamard_block, g)
+    check_codes(host(hp.c8), k1c, pre1, n, 8)
+    check_headers(host(hp.s8), k1s)
+    r2 = oracle.dequant_reduce([k1c[p * M:(p + 1) * M] for p in range(P)],
+                               [k1s[p * M // g:(p + 1) * M // g] for p in range(P)], M, 8, g, 4)
+    check_codes(host(hp.c4), r2["codes"], r2["pre"], M, 4)
+    r3 = oracle.dequant_reduce([r2["codes"][q * m // 2:(q + 1) * m // 2] for q in range(Q)],
+                               [r2["scales"][q * m // g:(q + 1) * m // g] for q in range(Q)], m, 4, g, 0,
+                               w.hadamard_block, 1.0 / (P * Q))
+    check_f32(host(hp.out), r3["f32"])
