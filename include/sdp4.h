@@ -183,7 +183,7 @@ int sdp4_dequant_reduce(int P, const void *const *codes, const float *const *sca
 
 /*
  * Standalone blockwise Hadamard transform (the unfused "HS w/o fused"
- * variant of Table 4, Sec. 5.3): y = (H_n / sqrt(n)) x per block.
+ * variant of Table 4, Sec. 5.4): y = (H_n / sqrt(n)) x per block.
  *   x, y [n] float32   y == x (in place) is allowed; partial overlap is not
  *   block              power of two in [2, 1024]; n a multiple of it
  * Errors: EINVAL, EALIGN, EHIP.

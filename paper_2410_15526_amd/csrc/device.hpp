@@ -94,18 +94,25 @@ SDP4_DEV int swz(int c)
         return c ^ ((c >> 3) & 7);
 }
 
-// Global (coalesced) -> registers (lane-contiguous).  Chunks at or beyond
-// `valid` are not read and come back as zero.
+// Coalesced global loads of one tile: instruction i, lane l reads chunk
+// 64*i + l.  Chunks at or beyond `valid` are not read and are zero.
 template <int R>
-SDP4_DEV void stage_in(const u32x4 *__restrict__ g, int valid, u32x4 *lds, u32x4 (&out)[R])
+SDP4_DEV void gload(const u32x4 *__restrict__ g, int valid, u32x4 (&t)[R])
 {
     const int lane = lane_id();
-    u32x4 t[R];
 #pragma unroll
     for (int i = 0; i < R; ++i) {
         const int c = kWave * i + lane;
         t[i] = c < valid ? __builtin_nontemporal_load(g + c) : u32x4{0u, 0u, 0u, 0u};
     }
+}
+
+// Coalesced chunks -> lane-contiguous chunks (lane l gets chunks R*l .. R*l+R-1)
+// through the wave's LDS region.
+template <int R>
+SDP4_DEV void transpose_in(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R])
+{
+    const int lane = lane_id();
 #pragma unroll
     for (int i = 0; i < R; ++i)
         lds[swz<R>(kWave * i + lane)] = t[i];
@@ -114,6 +121,15 @@ SDP4_DEV void stage_in(const u32x4 *__restrict__ g, int valid, u32x4 *lds, u32x4
     for (int k = 0; k < R; ++k)
         out[k] = lds[swz<R>(R * lane + k)];
     wave_lds_sync();
+}
+
+// Global (coalesced) -> registers (lane-contiguous).
+template <int R>
+SDP4_DEV void stage_in(const u32x4 *__restrict__ g, int valid, u32x4 *lds, u32x4 (&out)[R])
+{
+    u32x4 t[R];
+    gload<R>(g, valid, t);
+    transpose_in<R>(t, lds, out);
 }
 
 // Registers (lane-contiguous) -> global (coalesced).  Chunks at or beyond
@@ -212,28 +228,27 @@ SDP4_DEV void fwht_cross(float (&v)[E])
     }
 }
 
-template <int E>
-SDP4_DEV void fwht_lane(float (&v)[E], int nblk, float cn)
+template <int E, int NB>
+SDP4_DEV void fwht_lane(float (&v)[E], float cn)
 {
+    static_assert(NB >= 2 && (NB & (NB - 1)) == 0 && NB <= 64 * E, "block");
 #pragma unroll
-    for (int h = 1; h < E; h <<= 1) {
-        if (h < nblk) {
+    for (int h = 1; h < E && h < NB; h <<= 1) {
 #pragma unroll
-            for (int i = 0; i < E; ++i) {
-                if (i & h)
-                    continue;
-                const float a = v[i], b = v[i + h];
-                v[i] = a + b;
-                v[i + h] = a - b;
-            }
+        for (int i = 0; i < E; ++i) {
+            if (i & h)
+                continue;
+            const float a = v[i], b = v[i + h];
+            v[i] = a + b;
+            v[i + h] = a - b;
         }
     }
-    if (nblk > E) fwht_cross<E, 1>(v);
-    if (nblk > 2 * E) fwht_cross<E, 2>(v);
-    if (nblk > 4 * E) fwht_cross<E, 4>(v);
-    if (nblk > 8 * E) fwht_cross<E, 8>(v);
-    if (nblk > 16 * E) fwht_cross<E, 16>(v);
-    if (nblk > 32 * E) fwht_cross<E, 32>(v);
+    if constexpr (NB > E) fwht_cross<E, 1>(v);
+    if constexpr (NB > 2 * E) fwht_cross<E, 2>(v);
+    if constexpr (NB > 4 * E) fwht_cross<E, 4>(v);
+    if constexpr (NB > 8 * E) fwht_cross<E, 8>(v);
+    if constexpr (NB > 16 * E) fwht_cross<E, 16>(v);
+    if constexpr (NB > 32 * E) fwht_cross<E, 32>(v);
 #pragma unroll
     for (int i = 0; i < E; ++i)
         v[i] = v[i] * cn;

@@ -1,0 +1,47 @@
+// k_grad.hip -- launchers of the Hadamard + quantization kernel (K1) and of
+// the standalone Hadamard transform.
+#include "kernels.hpp"
+
+namespace sdp4 {
+
+namespace {
+
+template <int NB>
+struct GradQuant {
+    static int run(const float *x, int64_t n, int bits, int group, float cn, uint8_t *codes, float *scale,
+                   hipStream_t s)
+    {
+        if (group > 64 * 32) {
+            auto k = bits == 8 ? k_grad_quant<8, 64, NB, kPipe> : k_grad_quant<4, 64, NB, kPipe>;
+            return launch(k, wave_blocks(n, 64), kCap, s, x, n, group, cn, codes, scale);
+        }
+        auto k = bits == 8 ? k_grad_quant<8, 32, NB, kPipe> : k_grad_quant<4, 32, NB, kPipe>;
+        return launch(k, wave_blocks(n, 32), kCap, s, x, n, group, cn, codes, scale);
+    }
+};
+
+template <int NB>
+struct Hadamard {
+    static int run(const float *x, float *y, int64_t n, float cn, hipStream_t s)
+    {
+        if constexpr (NB < 2)
+            return 1;
+        else
+            return launch(k_hadamard<32, NB, kPipe>, wave_blocks(n, 32), kCap, s, x, y, n, cn);
+    }
+};
+
+} // namespace
+
+int launch_grad_quant(const float *x, int64_t n, int bits, int nblk, int group, float cn,
+                      uint8_t *codes, float *scale, hipStream_t s)
+{
+    return with_block<GradQuant>(nblk, x, n, bits, group, cn, codes, scale, s);
+}
+
+int launch_hadamard(const float *x, float *y, int64_t n, int nblk, float cn, hipStream_t s)
+{
+    return with_block<Hadamard>(nblk, x, y, n, cn, s);
+}
+
+} // namespace sdp4

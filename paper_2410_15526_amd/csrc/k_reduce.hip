@@ -1,0 +1,96 @@
+// k_reduce.hip -- launchers of the dequantize-reduce kernel with 4- or
+// 8-bit re-quantization (K2), and of the float32 reduction and the copy.
+#include "kernels.hpp"
+
+namespace sdp4 {
+
+// ---------------------------------------------------------------------------
+// standalone float32 reduction and plain copy (16 bytes per lane per step)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlockThreads) void k_reduce_f32(F32Table xs, int P, int64_t n,
+                                                               float *__restrict__ y)
+{
+    const int64_t n4 = n / 4;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+        float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+        for (int p = 0; p < P; ++p) {
+            const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(xs.p[p]) + i);
+            a0 = a0 + __uint_as_float(v.x);
+            a1 = a1 + __uint_as_float(v.y);
+            a2 = a2 + __uint_as_float(v.z);
+            a3 = a3 + __uint_as_float(v.w);
+        }
+        __builtin_nontemporal_store(u32x4{__float_as_uint(a0), __float_as_uint(a1), __float_as_uint(a2),
+                                          __float_as_uint(a3)},
+                                    reinterpret_cast<u32x4 *>(y) + i);
+    }
+    for (int64_t i = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        float a = 0.0f;
+        for (int p = 0; p < P; ++p)
+            a = a + xs.p[p][i];
+        y[i] = a;
+    }
+}
+
+// Block-contiguous copy: each block moves 16 KiB per iteration with four
+// 16-byte loads per lane in flight.
+__global__ __launch_bounds__(kBlockThreads) void k_copy_f32(const float *__restrict__ x,
+                                                             float *__restrict__ y, int64_t n)
+{
+    constexpr int U = 4;
+    const int64_t n4 = n / 4;
+    const int64_t chunk = (int64_t)kBlockThreads * U;
+    const int64_t nchunks = n4 / chunk;
+    const u32x4 *xv = reinterpret_cast<const u32x4 *>(x);
+    u32x4 *yv = reinterpret_cast<u32x4 *>(y);
+    for (int64_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            v[u] = __builtin_nontemporal_load(xv + c * chunk + u * kBlockThreads + threadIdx.x);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            __builtin_nontemporal_store(v[u], yv + c * chunk + u * kBlockThreads + threadIdx.x);
+    }
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = nchunks * chunk * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        y[i] = x[i];
+}
+
+int launch_dequant_reduce(const PeerTable &peers, int P, int64_t n, int bits_in, int group,
+                          int bits_out, int nblk, float cn, float out_scale, uint8_t *out_codes,
+                          float *out_scales, float *out_f32, hipStream_t s)
+{
+    if (bits_out == 0)
+        return bits_in == 8
+                   ? launch_dequant_reduce_f32_in8(peers, P, n, group, nblk, cn, out_scale, out_f32, s)
+                   : launch_dequant_reduce_f32_in4(peers, P, n, group, nblk, cn, out_scale, out_f32, s);
+    const bool wide = group > 64 * 32;
+    if (bits_in == 8) {
+        if (bits_out == 4)
+            return wide ? dr_launch<8, 4, 64, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s)
+                        : dr_launch<8, 4, 32, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s);
+        return wide ? dr_launch<8, 8, 64, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s)
+                    : dr_launch<8, 8, 32, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s);
+    }
+    if (bits_out == 4)
+        return wide ? dr_launch<4, 4, 64, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s)
+                    : dr_launch<4, 4, 32, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s);
+    return wide ? dr_launch<4, 8, 64, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s)
+                : dr_launch<4, 8, 32, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s);
+}
+
+int launch_reduce_f32(const F32Table &xs, int P, int64_t n, float *y, hipStream_t s)
+{
+    const int64_t blocks = (n / 4 + kBlockThreads - 1) / kBlockThreads;
+    return launch(k_reduce_f32, blocks > 0 ? blocks : 1, 0, s, xs, P, n, y);
+}
+
+int launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s)
+{
+    const int64_t chunks = n / 4 / (kBlockThreads * 4);
+    return launch(k_copy_f32, chunks > 0 ? chunks : 1, 2, s, x, y, n);
+}
+
+} // namespace sdp4

@@ -1,0 +1,492 @@
+// kernels.hpp -- gfx950 kernel templates of the SDP4Bit compression hot
+// path; the .hip files instantiate and launch them.
+//
+//
+// Every kernel is a persistent loop of wavefronts over wave tiles of 64*E
+// consecutive elements (see device.hpp for the lane layout).  Blocks have
+// four independent wavefronts, each with its own LDS staging region; no
+// kernel needs a block-wide barrier.  With PIPE set, a wave issues the
+// global loads of its next tile before it processes the current one, so
+// HBM latency overlaps the LDS transposes, the arithmetic and the stores.
+// Everything a wave computes for a tile depends on that tile alone, so
+// results do not depend on the grid size or on the pipelining.
+#pragma once
+
+#include "device.hpp"
+#include "launch.hpp"
+
+#ifndef SDP4_PIPE
+#define SDP4_PIPE 1
+#endif
+#ifndef SDP4_BLOCKS_PER_CU
+#define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
+#endif
+
+namespace sdp4 {
+
+constexpr bool kPipe = SDP4_PIPE != 0;
+
+template <bool PIPE, class Tile, class Load, class Proc>
+SDP4_DEV void tile_loop(int64_t ntiles, Load load, Proc proc)
+{
+    const int wave = threadIdx.x / kWave;
+    const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
+    int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+    if constexpr (!PIPE) {
+        for (; t < ntiles; t += stride) {
+            Tile in;
+            load(t, in);
+            proc(t, in);
+        }
+    } else {
+        if (t >= ntiles)
+            return;
+        Tile cur;
+        load(t, cur);
+        for (;;) {
+            const int64_t tn = t + stride;
+            if (tn < ntiles) {
+                Tile nxt;
+                load(tn, nxt);
+                proc(t, cur);
+                cur = nxt;
+                t = tn;
+            } else {
+                proc(t, cur);
+                break;
+            }
+        }
+    }
+}
+
+SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base < W ? n - base : W); }
+
+template <int E, int NB>
+SDP4_DEV void maybe_fwht(float (&v)[E], float cn)
+{
+    if constexpr (NB > 1)
+        fwht_lane<E, NB>(v, cn);
+}
+
+// ---------------------------------------------------------------------------
+// qWD encode: d = w_new - widen(w_prev); asymmetric 4-bit codes per group
+// ---------------------------------------------------------------------------
+template <bool BF16, int E, bool PIPE>
+__global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
+    const float *__restrict__ w_new, const void *__restrict__ w_prev, int64_t n, int group,
+    uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv)
+{
+    constexpr int W = kWave * E;
+    constexpr int R = E / 4;                       // f32 chunks per lane
+    constexpr int RP = BF16 ? E / 8 : E / 4;       // previous-weight chunks per lane
+    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    u32x4 *lds = lds_all[threadIdx.x / kWave];
+    const int lane = lane_id();
+    const int lanes_per_group = group / E;
+    struct Tile {
+        u32x4 a[R];
+        u32x4 b[RP];
+    };
+    auto load = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        const int valid = tile_valid(n, base, W);
+        gload<R>(reinterpret_cast<const u32x4 *>(w_new + base), valid / 4, in.a);
+        if constexpr (BF16)
+            gload<RP>(reinterpret_cast<const u32x4 *>(static_cast<const uint16_t *>(w_prev) + base), valid / 8,
+                      in.b);
+        else
+            gload<RP>(reinterpret_cast<const u32x4 *>(static_cast<const float *>(w_prev) + base), valid / 4,
+                      in.b);
+    };
+    auto proc = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        const int valid = tile_valid(n, base, W);
+        float d[E], p[E];
+        {
+            u32x4 c[R];
+            transpose_in<R>(in.a, lds, c);
+            chunks_to_f32<E>(c, d);
+        }
+        {
+            u32x4 c[RP];
+            transpose_in<RP>(in.b, lds, c);
+            if constexpr (BF16)
+                bf16_chunks_to_f32<E>(c, p);
+            else
+                chunks_to_f32<E>(c, p);
+        }
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+            d[i] = d[i] - p[i];
+        float mn = d[0], mx = d[0];
+#pragma unroll
+        for (int i = 1; i < E; ++i) {
+            mn = fminf(mn, d[i]);
+            mx = fmaxf(mx, d[i]);
+        }
+        minmax_lanes(mn, mx, lanes_per_group);
+        const float range = mx - mn;
+        const float r = 15.0f / range;
+        const bool degenerate = !(range > 0.0f) || !__builtin_isfinite(range) || !__builtin_isfinite(r);
+        const float s = degenerate ? 0.0f : range / 15.0f;
+        const float inv = degenerate ? 0.0f : r;
+        int q[E];
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+            q[i] = (int)__builtin_amdgcn_fmed3f(__builtin_rintf((d[i] - mn) * inv), 0.0f, 15.0f);
+        u32x4 pk[E / 32];
+        pack4<E>(q, pk);
+        const int off = E * lane;
+        if (off < valid) {
+            u32x4 *dst = reinterpret_cast<u32x4 *>(codes + (base + off) / 2);
+#pragma unroll
+            for (int k = 0; k < E / 32; ++k)
+                __builtin_nontemporal_store(pk[k], dst + k);
+            if (off % group == 0) {
+                const int64_t gi = (base + off) / group;
+                scale[gi] = s;
+                minv[gi] = mn;
+            }
+        }
+    };
+    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+}
+
+// ---------------------------------------------------------------------------
+// qWD decode: w_prev <- narrow(widen(w_prev) + fma(code, scale, min))
+// ---------------------------------------------------------------------------
+template <bool BF16, int E, bool PIPE>
+__global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
+    const uint8_t *__restrict__ codes, const float *__restrict__ scale,
+    const float *__restrict__ minv, int64_t n, int group, void *__restrict__ w_prev)
+{
+    constexpr int W = kWave * E;
+    constexpr int RP = BF16 ? E / 8 : E / 4;
+    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * (E / 4)];
+    u32x4 *lds = lds_all[threadIdx.x / kWave];
+    const int lane = lane_id();
+    struct Tile {
+        u32x4 c[E / 32];
+        float s, mn;
+        u32x4 w[RP];
+    };
+    auto load = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        const int valid = tile_valid(n, base, W);
+        const int off = E * lane;
+        if (off < valid) {
+            const u32x4 *src = reinterpret_cast<const u32x4 *>(codes + (base + off) / 2);
+#pragma unroll
+            for (int k = 0; k < E / 32; ++k)
+                in.c[k] = __builtin_nontemporal_load(src + k);
+            const int64_t gi = (base + off) / group;
+            in.s = scale[gi];
+            in.mn = minv[gi];
+        } else {
+#pragma unroll
+            for (int k = 0; k < E / 32; ++k)
+                in.c[k] = u32x4{0u, 0u, 0u, 0u};
+            in.s = 0.0f;
+            in.mn = 0.0f;
+        }
+        if constexpr (BF16)
+            gload<RP>(reinterpret_cast<const u32x4 *>(static_cast<const uint16_t *>(w_prev) + base), valid / 8,
+                      in.w);
+        else
+            gload<RP>(reinterpret_cast<const u32x4 *>(static_cast<const float *>(w_prev) + base), valid / 4,
+                      in.w);
+    };
+    auto proc = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        const int valid = tile_valid(n, base, W);
+        float w[E];
+        u32x4 c[RP];
+        transpose_in<RP>(in.w, lds, c);
+        if constexpr (BF16)
+            bf16_chunks_to_f32<E>(c, w);
+        else
+            chunks_to_f32<E>(c, w);
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            const uint32_t word = in.c[i / 32][(i / 8) % 4];
+            const float code = (float)((word >> (4 * (i % 8))) & 0xFu);
+            w[i] = w[i] + __builtin_fmaf(code, in.s, in.mn);
+        }
+        if constexpr (BF16) {
+            f32_to_bf16_chunks<E>(w, c);
+            stage_out<RP>(reinterpret_cast<u32x4 *>(static_cast<uint16_t *>(w_prev) + base), valid / 8, lds, c);
+        } else {
+            f32_to_chunks<E>(w, c);
+            stage_out<RP>(reinterpret_cast<u32x4 *>(static_cast<float *>(w_prev) + base), valid / 4, lds, c);
+        }
+    };
+    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+}
+
+// ---------------------------------------------------------------------------
+// K1: blockwise Hadamard (block NB, 0 = none) + symmetric BITS-bit group quantization
+// ---------------------------------------------------------------------------
+template <int BITS, int E, int NB, bool PIPE>
+__global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
+    const float *__restrict__ x, int64_t n, int group, float cn, uint8_t *__restrict__ codes,
+    float *__restrict__ scale)
+{
+    constexpr int W = kWave * E;
+    constexpr int R = E / 4;
+    constexpr float qmax = BITS == 8 ? 127.0f : 7.0f;
+    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    u32x4 *lds = lds_all[threadIdx.x / kWave];
+    const int lane = lane_id();
+    const int lanes_per_group = group / E;
+    struct Tile {
+        u32x4 a[R];
+    };
+    auto load = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        gload<R>(reinterpret_cast<const u32x4 *>(x + base), tile_valid(n, base, W) / 4, in.a);
+    };
+    auto proc = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        const int valid = tile_valid(n, base, W);
+        float v[E];
+        {
+            u32x4 c[R];
+            transpose_in<R>(in.a, lds, c);
+            chunks_to_f32<E>(c, v);
+        }
+        maybe_fwht<E, NB>(v, cn);
+        float a = 0.0f;
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+            a = fmaxf(a, fabsf(v[i]));
+        max_lanes<E>(a, lanes_per_group);
+        float s, inv;
+        sym_params(a, qmax, s, inv);
+        int q[E];
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+            q[i] = quant_sym1(v[i], inv, qmax);
+        const int off = E * lane;
+        if (off < valid) {
+            if constexpr (BITS == 8) {
+                u32x4 pk[E / 16];
+                pack8<E>(q, pk);
+                u32x4 *dst = reinterpret_cast<u32x4 *>(codes + base + off);
+#pragma unroll
+                for (int k = 0; k < E / 16; ++k)
+                    __builtin_nontemporal_store(pk[k], dst + k);
+            } else {
+                u32x4 pk[E / 32];
+                pack4<E>(q, pk);
+                u32x4 *dst = reinterpret_cast<u32x4 *>(codes + (base + off) / 2);
+#pragma unroll
+                for (int k = 0; k < E / 32; ++k)
+                    __builtin_nontemporal_store(pk[k], dst + k);
+            }
+            if (off % group == 0)
+                scale[(base + off) / group] = s;
+        }
+    };
+    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+}
+
+// ---------------------------------------------------------------------------
+// K2 / K3: dequantize + reduce over P <= PMAX chunks, then re-quantize
+// (BITS_OUT 4/8) or inverse Hadamard (block NB) + out_scale to float32
+// (BITS_OUT 0)
+// ---------------------------------------------------------------------------
+template <int BITS_IN, int BITS_OUT, int E, int NB, int PMAX, bool PIPE>
+__global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
+    PeerTable peers, int P, int64_t n, int group, float cn, float out_scale, uint8_t *__restrict__ out_codes,
+    float *__restrict__ out_scales, float *__restrict__ out_f32)
+{
+    constexpr int W = kWave * E;
+    constexpr int R = E / 4;
+    constexpr int CW = E * BITS_IN / 128; // input chunks (16 B) per lane per peer
+    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    u32x4 *lds = lds_all[threadIdx.x / kWave];
+    const int lane = lane_id();
+    struct Tile {
+        u32x4 c[PMAX][CW];
+        float s[PMAX];
+    };
+    auto load = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        const int off = E * lane;
+        const bool active = off < tile_valid(n, base, W);
+        const int64_t gi = (base + off) / group;
+#pragma unroll
+        for (int j = 0; j < PMAX; ++j) {
+            if (j < P && active) {
+                const u32x4 *src = reinterpret_cast<const u32x4 *>(
+                    static_cast<const uint8_t *>(peers.codes[j]) + (base + off) * BITS_IN / 8);
+#pragma unroll
+                for (int k = 0; k < CW; ++k)
+                    in.c[j][k] = __builtin_nontemporal_load(src + k);
+                in.s[j] = peers.scales[j][gi];
+            } else {
+#pragma unroll
+                for (int k = 0; k < CW; ++k)
+                    in.c[j][k] = u32x4{0u, 0u, 0u, 0u};
+                in.s[j] = 0.0f;
+            }
+        }
+    };
+    auto proc = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        const int valid = tile_valid(n, base, W);
+        const int off = E * lane;
+        float acc[E];
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+            acc[i] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < PMAX; ++j) {
+            if (j < P) {
+                uint32_t w[CW * 4];
+#pragma unroll
+                for (int k = 0; k < CW; ++k) {
+                    w[4 * k] = in.c[j][k].x;
+                    w[4 * k + 1] = in.c[j][k].y;
+                    w[4 * k + 2] = in.c[j][k].z;
+                    w[4 * k + 3] = in.c[j][k].w;
+                }
+#pragma unroll
+                for (int i = 0; i < E; ++i)
+                    acc[i] = __builtin_fmaf(code_f<BITS_IN>(w, i), in.s[j], acc[i]);
+            }
+        }
+        if constexpr (BITS_OUT == 0) {
+            maybe_fwht<E, NB>(acc, cn);
+            if (out_scale != 1.0f) {
+#pragma unroll
+                for (int i = 0; i < E; ++i)
+                    acc[i] = acc[i] * out_scale;
+            }
+            u32x4 c[R];
+            f32_to_chunks<E>(acc, c);
+            stage_out<R>(reinterpret_cast<u32x4 *>(out_f32 + base), valid / 4, lds, c);
+        } else {
+            if (out_f32) {
+                u32x4 c[R];
+                f32_to_chunks<E>(acc, c);
+                stage_out<R>(reinterpret_cast<u32x4 *>(out_f32 + base), valid / 4, lds, c);
+            }
+            constexpr float qmax = BITS_OUT == 8 ? 127.0f : 7.0f;
+            float a = 0.0f;
+#pragma unroll
+            for (int i = 0; i < E; ++i)
+                a = fmaxf(a, fabsf(acc[i]));
+            max_lanes<E>(a, group / E);
+            float s, inv;
+            sym_params(a, qmax, s, inv);
+            int q[E];
+#pragma unroll
+            for (int i = 0; i < E; ++i)
+                q[i] = quant_sym1(acc[i], inv, qmax);
+            if (off < valid) {
+                if constexpr (BITS_OUT == 8) {
+                    u32x4 pk[E / 16];
+                    pack8<E>(q, pk);
+                    u32x4 *dst = reinterpret_cast<u32x4 *>(out_codes + base + off);
+#pragma unroll
+                    for (int k = 0; k < E / 16; ++k)
+                        __builtin_nontemporal_store(pk[k], dst + k);
+                } else {
+                    u32x4 pk[E / 32];
+                    pack4<E>(q, pk);
+                    u32x4 *dst = reinterpret_cast<u32x4 *>(out_codes + (base + off) / 2);
+#pragma unroll
+                    for (int k = 0; k < E / 32; ++k)
+                        __builtin_nontemporal_store(pk[k], dst + k);
+                }
+                if (off % group == 0)
+                    out_scales[(base + off) / group] = s;
+            }
+        }
+    };
+    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+}
+
+// ---------------------------------------------------------------------------
+// standalone Hadamard (unfused variant); in place allowed
+// ---------------------------------------------------------------------------
+template <int E, int NB, bool PIPE>
+__global__ __launch_bounds__(kBlockThreads) void k_hadamard(const float *x, float *y, int64_t n, float cn)
+{
+    constexpr int W = kWave * E;
+    constexpr int R = E / 4;
+    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    u32x4 *lds = lds_all[threadIdx.x / kWave];
+    struct Tile {
+        u32x4 a[R];
+    };
+    // In place, a prefetched tile is never one a previous iteration wrote
+    // (each wave only ever touches its own tiles), so prefetching is safe.
+    auto load = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        gload<R>(reinterpret_cast<const u32x4 *>(x + base), tile_valid(n, base, W) / 4, in.a);
+    };
+    auto proc = [&](int64_t t, Tile &in) {
+        const int64_t base = t * W;
+        u32x4 c[R];
+        transpose_in<R>(in.a, lds, c);
+        float v[E];
+        chunks_to_f32<E>(c, v);
+        fwht_lane<E, NB>(v, cn);
+        f32_to_chunks<E>(v, c);
+        stage_out<R>(reinterpret_cast<u32x4 *>(y + base), tile_valid(n, base, W) / 4, lds, c);
+    };
+    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+}
+
+// ---------------------------------------------------------------------------
+// launch helpers shared by the .hip translation units
+// ---------------------------------------------------------------------------
+inline int64_t wave_blocks(int64_t n, int E)
+{
+    const int64_t W = (int64_t)kWave * E;
+    const int64_t tiles = (n + W - 1) / W;
+    return (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+}
+
+constexpr int kCap = SDP4_BLOCKS_PER_CU;
+static_assert(kBlockThreads == kLaunchThreads, "block size");
+
+// Hadamard block sizes the kernels are compiled for: 0 (none), 2 .. 1024.
+template <template <int> class F, typename... A>
+int with_block(int nb, A... a)
+{
+    switch (nb) {
+    case 0: return F<0>::run(a...);
+    case 2: return F<2>::run(a...);
+    case 4: return F<4>::run(a...);
+    case 8: return F<8>::run(a...);
+    case 16: return F<16>::run(a...);
+    case 32: return F<32>::run(a...);
+    case 64: return F<64>::run(a...);
+    case 128: return F<128>::run(a...);
+    case 256: return F<256>::run(a...);
+    case 512: return F<512>::run(a...);
+    case 1024: return F<1024>::run(a...);
+    default: return 1;
+    }
+}
+
+// Peer counts 1..16: loads of up to 8 peers are batched (and prefetched);
+// more than 8 peers use a 16-wide batch without prefetch.
+template <int BITS_IN, int BITS_OUT, int E, int NB>
+int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, float out_scale,
+              uint8_t *out_codes, float *out_scales, float *out_f32, hipStream_t s)
+{
+    if (P <= 4)
+        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, kPipe>, wave_blocks(n, E), kCap, s, peers, P,
+                      n, group, cn, out_scale, out_codes, out_scales, out_f32);
+    if (P <= 8)
+        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, kPipe>, wave_blocks(n, E), kCap, s, peers, P,
+                      n, group, cn, out_scale, out_codes, out_scales, out_f32);
+    return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, false>, wave_blocks(n, E), kCap, s, peers, P, n,
+                  group, cn, out_scale, out_codes, out_scales, out_f32);
+}
+
+} // namespace sdp4

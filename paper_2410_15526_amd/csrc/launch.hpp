@@ -1,13 +1,16 @@
 // launch.hpp -- interface between the C ABI layer (abi.cpp) and the kernel
-// launchers (kernels.hip).  Launchers assume validated arguments.
+// launchers (*.hip).  Launchers assume validated arguments.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include <tuple>
+
 namespace sdp4 {
 
 constexpr int kMaxPeers = 16;
+constexpr int kLaunchThreads = 256;
 
 // Pointer tables passed by value in the kernel arguments.
 struct PeerTable {
@@ -21,6 +24,31 @@ struct F32Table {
 // Records `err` as the calling thread's last HIP error and returns SDP4_EHIP.
 int set_hip_error(hipError_t err);
 
+// Grid of a persistent kernel: the blocks of `kernel` that are resident at
+// once on the current device (capped at per_cu_cap per compute unit when
+// per_cu_cap > 0), and never more than nwork_blocks.
+int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, hipError_t &err);
+
+template <typename... Params, typename... Args>
+int launch(void (*kernel)(Params...), int64_t nwork_blocks, int per_cu_cap, hipStream_t stream, Args... args)
+{
+    hipError_t err;
+    const int grid = grid_for(reinterpret_cast<const void *>(kernel), nwork_blocks, per_cu_cap, err);
+    if (err != hipSuccess)
+        return set_hip_error(err);
+    std::tuple<Params...> values(args...);
+    void *argv[sizeof...(Params)];
+    std::apply([&](auto &...v) {
+        int i = 0;
+        ((argv[i++] = static_cast<void *>(&v)), ...);
+    }, values);
+    err = hipLaunchKernel(reinterpret_cast<const void *>(kernel), dim3(grid), dim3(kLaunchThreads), argv, 0,
+                          stream);
+    if (err != hipSuccess)
+        return set_hip_error(err);
+    return 0;
+}
+
 int launch_qwd_encode(const float *w_new, const void *w_prev, bool bf16, int64_t n, int group,
                       uint8_t *codes, float *scale, float *minv, hipStream_t s);
 int launch_qwd_decode(const uint8_t *codes, const float *scale, const float *minv, int64_t n,
@@ -30,6 +58,10 @@ int launch_grad_quant(const float *x, int64_t n, int bits, int nblk, int group, 
 int launch_dequant_reduce(const PeerTable &peers, int P, int64_t n, int bits_in, int group,
                           int bits_out, int nblk, float cn, float out_scale, uint8_t *out_codes,
                           float *out_scales, float *out_f32, hipStream_t s);
+int launch_dequant_reduce_f32_in8(const PeerTable &peers, int P, int64_t n, int group, int nblk, float cn,
+                                  float out_scale, float *out_f32, hipStream_t s);
+int launch_dequant_reduce_f32_in4(const PeerTable &peers, int P, int64_t n, int group, int nblk, float cn,
+                                  float out_scale, float *out_f32, hipStream_t s);
 int launch_hadamard(const float *x, float *y, int64_t n, int nblk, float cn, hipStream_t s);
 int launch_reduce_f32(const F32Table &xs, int P, int64_t n, float *y, hipStream_t s);
 int launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s);
