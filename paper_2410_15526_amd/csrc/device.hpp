@@ -266,45 +266,58 @@ SDP4_DEV void sym_params(float a, float qmax, float &scale, float &inv)
     inv = degenerate ? 0.0f : r;
 }
 
-SDP4_DEV int quant_sym1(float x, float inv, float qmax)
+// Code bits of one element: fl(x * inv) rounded to the nearest integer,
+// ties to even, and returned in the low bits of a word.  Adding 1.5 * 2^23
+// to a float of magnitude below 2^22 rounds it to an integer in round-to-
+// nearest-even mode (exactly what rint does) and leaves that integer,
+// two's complement, in the low mantissa bits.  No clamp is needed: with
+// inv = fl(qmax / s) and |x| <= s, |fl(x * inv)| <= fl(qmax (1 + 2^-24)),
+// which rounds to at most qmax (and likewise 0..15 for the asymmetric
+// case, where 0 <= fl(x - mn) <= fl(mx - mn)).
+constexpr float kRoundMagic = 12582912.0f; // 1.5 * 2^23
+
+SDP4_DEV uint32_t code_bits(float x, float inv)
 {
-    const float r = __builtin_rintf(x * inv);
-    return (int)__builtin_amdgcn_fmed3f(r, -qmax, qmax);
+    const float v = x * inv;
+    return __float_as_uint(v + kRoundMagic);
 }
 
-// E codes -> E bytes (int8) as E/16 chunks
+// low bytes of t0..t3 -> one word, t0 in the lowest byte
+SDP4_DEV uint32_t pack_bytes4(uint32_t t0, uint32_t t1, uint32_t t2, uint32_t t3)
+{
+    const uint32_t lo = __builtin_amdgcn_perm(t1, t0, 0x0C0C0400u); // t0.b0, t1.b0
+    const uint32_t hi = __builtin_amdgcn_perm(t3, t2, 0x0C0C0400u); // t2.b0, t3.b0
+    return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+}
+
+// E code words -> E bytes (int8) as E/16 chunks
 template <int E>
-SDP4_DEV void pack8(const int (&q)[E], u32x4 (&c)[E / 16])
+SDP4_DEV void pack8(const uint32_t (&t)[E], u32x4 (&c)[E / 16])
 {
 #pragma unroll
     for (int k = 0; k < E / 16; ++k) {
-        uint32_t w[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int *p = q + 16 * k + 4 * j;
-            w[j] = (uint32_t)(p[0] & 0xFF) | ((uint32_t)(p[1] & 0xFF) << 8) |
-                   ((uint32_t)(p[2] & 0xFF) << 16) | ((uint32_t)p[3] << 24);
-        }
-        c[k] = u32x4{w[0], w[1], w[2], w[3]};
+        const uint32_t *p = t + 16 * k;
+        c[k] = u32x4{pack_bytes4(p[0], p[1], p[2], p[3]), pack_bytes4(p[4], p[5], p[6], p[7]),
+                     pack_bytes4(p[8], p[9], p[10], p[11]), pack_bytes4(p[12], p[13], p[14], p[15])};
     }
 }
 
-// E codes -> E/2 bytes (nibbles, even element low) as E/32 chunks
+// 8 code words -> 8 nibbles, element 0 in the lowest nibble
+SDP4_DEV uint32_t pack_nibbles8(const uint32_t *p)
+{
+    const uint32_t ev = pack_bytes4(p[0], p[2], p[4], p[6]);
+    const uint32_t od = pack_bytes4(p[1], p[3], p[5], p[7]);
+    return (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+}
+
+// E code words -> E/2 bytes (nibbles, even element low) as E/32 chunks
 template <int E>
-SDP4_DEV void pack4(const int (&q)[E], u32x4 (&c)[E / 32])
+SDP4_DEV void pack4(const uint32_t (&t)[E], u32x4 (&c)[E / 32])
 {
 #pragma unroll
     for (int k = 0; k < E / 32; ++k) {
-        uint32_t w[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            uint32_t acc = 0;
-#pragma unroll
-            for (int m = 0; m < 8; ++m)
-                acc |= (uint32_t)(q[32 * k + 8 * j + m] & 0xF) << (4 * m);
-            w[j] = acc;
-        }
-        c[k] = u32x4{w[0], w[1], w[2], w[3]};
+        const uint32_t *p = t + 32 * k;
+        c[k] = u32x4{pack_nibbles8(p), pack_nibbles8(p + 8), pack_nibbles8(p + 16), pack_nibbles8(p + 24)};
     }
 }
 

@@ -18,6 +18,9 @@
 #ifndef SDP4_PIPE
 #define SDP4_PIPE 1
 #endif
+#ifndef SDP4_PEER_LDS
+#define SDP4_PEER_LDS 1
+#endif
 #ifndef SDP4_BLOCKS_PER_CU
 #define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
 #endif
@@ -60,6 +63,26 @@ SDP4_DEV void tile_loop(int64_t ntiles, Load load, Proc proc)
 }
 
 SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base < W ? n - base : W); }
+
+// Store the packed codes of a tile (lane l owns bytes [l*E*BITS/8, ...)):
+// one 16-byte chunk per lane goes out directly; more go through the wave's
+// LDS region so that every store instruction writes 1 KiB contiguous.
+template <int E, int BITS>
+SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, const uint32_t (&q)[E])
+{
+    constexpr int RC = E * BITS / 128; // 16-byte chunks per lane
+    u32x4 pk[RC];
+    if constexpr (BITS == 8)
+        pack8<E>(q, pk);
+    else
+        pack4<E>(q, pk);
+    if constexpr (RC == 1) {
+        if (E * lane_id() < valid)
+            __builtin_nontemporal_store(pk[0], reinterpret_cast<u32x4 *>(dst) + lane_id());
+    } else {
+        stage_out<RC>(reinterpret_cast<u32x4 *>(dst), valid * BITS / 128, lds, pk);
+    }
+}
 
 template <int E, int NB>
 SDP4_DEV void maybe_fwht(float (&v)[E], float cn)
@@ -130,23 +153,16 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
         const bool degenerate = !(range > 0.0f) || !__builtin_isfinite(range) || !__builtin_isfinite(r);
         const float s = degenerate ? 0.0f : range / 15.0f;
         const float inv = degenerate ? 0.0f : r;
-        int q[E];
+        uint32_t q[E];
 #pragma unroll
         for (int i = 0; i < E; ++i)
-            q[i] = (int)__builtin_amdgcn_fmed3f(__builtin_rintf((d[i] - mn) * inv), 0.0f, 15.0f);
-        u32x4 pk[E / 32];
-        pack4<E>(q, pk);
+            q[i] = code_bits(d[i] - mn, inv);
+        store_codes<E, 4>(codes + base / 2, valid, lds, q);
         const int off = E * lane;
-        if (off < valid) {
-            u32x4 *dst = reinterpret_cast<u32x4 *>(codes + (base + off) / 2);
-#pragma unroll
-            for (int k = 0; k < E / 32; ++k)
-                __builtin_nontemporal_store(pk[k], dst + k);
-            if (off % group == 0) {
-                const int64_t gi = (base + off) / group;
-                scale[gi] = s;
-                minv[gi] = mn;
-            }
+        if (off < valid && off % group == 0) {
+            const int64_t gi = (base + off) / group;
+            scale[gi] = s;
+            minv[gi] = mn;
         }
     };
     tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
@@ -262,30 +278,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
         max_lanes<E>(a, lanes_per_group);
         float s, inv;
         sym_params(a, qmax, s, inv);
-        int q[E];
+        uint32_t q[E];
 #pragma unroll
         for (int i = 0; i < E; ++i)
-            q[i] = quant_sym1(v[i], inv, qmax);
+            q[i] = code_bits(v[i], inv);
+        store_codes<E, BITS>(codes + base * BITS / 8, valid, lds, q);
         const int off = E * lane;
-        if (off < valid) {
-            if constexpr (BITS == 8) {
-                u32x4 pk[E / 16];
-                pack8<E>(q, pk);
-                u32x4 *dst = reinterpret_cast<u32x4 *>(codes + base + off);
-#pragma unroll
-                for (int k = 0; k < E / 16; ++k)
-                    __builtin_nontemporal_store(pk[k], dst + k);
-            } else {
-                u32x4 pk[E / 32];
-                pack4<E>(q, pk);
-                u32x4 *dst = reinterpret_cast<u32x4 *>(codes + (base + off) / 2);
-#pragma unroll
-                for (int k = 0; k < E / 32; ++k)
-                    __builtin_nontemporal_store(pk[k], dst + k);
-            }
-            if (off % group == 0)
-                scale[(base + off) / group] = s;
-        }
+        if (off < valid && off % group == 0)
+            scale[(base + off) / group] = s;
     };
     tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
 }
@@ -317,6 +317,15 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
         const int64_t gi = (base + off) / group;
 #pragma unroll
         for (int j = 0; j < PMAX; ++j) {
+            if constexpr (SDP4_PEER_LDS && CW > 1) {
+                if (j < P) {
+                    gload<CW>(reinterpret_cast<const u32x4 *>(static_cast<const uint8_t *>(peers.codes[j]) +
+                                                               base * BITS_IN / 8),
+                              tile_valid(n, base, W) * BITS_IN / 128, in.c[j]);
+                    in.s[j] = active ? peers.scales[j][gi] : 0.0f;
+                }
+                continue;
+            }
             if (j < P && active) {
                 const u32x4 *src = reinterpret_cast<const u32x4 *>(
                     static_cast<const uint8_t *>(peers.codes[j]) + (base + off) * BITS_IN / 8);
@@ -343,6 +352,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
 #pragma unroll
         for (int j = 0; j < PMAX; ++j) {
             if (j < P) {
+                if constexpr (SDP4_PEER_LDS && CW > 1) {
+                    u32x4 tmp[CW];
+                    transpose_in<CW>(in.c[j], lds, tmp);
+#pragma unroll
+                    for (int k = 0; k < CW; ++k)
+                        in.c[j][k] = tmp[k];
+                }
                 uint32_t w[CW * 4];
 #pragma unroll
                 for (int k = 0; k < CW; ++k) {
@@ -380,29 +396,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
             max_lanes<E>(a, group / E);
             float s, inv;
             sym_params(a, qmax, s, inv);
-            int q[E];
+            uint32_t q[E];
 #pragma unroll
             for (int i = 0; i < E; ++i)
-                q[i] = quant_sym1(acc[i], inv, qmax);
-            if (off < valid) {
-                if constexpr (BITS_OUT == 8) {
-                    u32x4 pk[E / 16];
-                    pack8<E>(q, pk);
-                    u32x4 *dst = reinterpret_cast<u32x4 *>(out_codes + base + off);
-#pragma unroll
-                    for (int k = 0; k < E / 16; ++k)
-                        __builtin_nontemporal_store(pk[k], dst + k);
-                } else {
-                    u32x4 pk[E / 32];
-                    pack4<E>(q, pk);
-                    u32x4 *dst = reinterpret_cast<u32x4 *>(out_codes + (base + off) / 2);
-#pragma unroll
-                    for (int k = 0; k < E / 32; ++k)
-                        __builtin_nontemporal_store(pk[k], dst + k);
-                }
-                if (off % group == 0)
-                    out_scales[(base + off) / group] = s;
-            }
+                q[i] = code_bits(acc[i], inv);
+            store_codes<E, BITS_OUT>(out_codes + base * BITS_OUT / 8, valid, lds, q);
+            if (off < valid && off % group == 0)
+                out_scales[(base + off) / group] = s;
         }
     };
     tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
@@ -475,15 +475,19 @@ int with_block(int nb, A... a)
 
 // Peer counts 1..16: loads of up to 8 peers are batched (and prefetched);
 // more than 8 peers use a 16-wide batch without prefetch.
+// The re-quantizing variant keeps P chunks per lane in flight already and
+// is fastest without the extra prefetch buffer (measured); the float32
+// variant prefetches.
 template <int BITS_IN, int BITS_OUT, int E, int NB>
 int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, float out_scale,
               uint8_t *out_codes, float *out_scales, float *out_f32, hipStream_t s)
 {
+    constexpr bool pipe = kPipe && BITS_OUT == 0;
     if (P <= 4)
-        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, kPipe>, wave_blocks(n, E), kCap, s, peers, P,
+        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe>, wave_blocks(n, E), kCap, s, peers, P,
                       n, group, cn, out_scale, out_codes, out_scales, out_f32);
     if (P <= 8)
-        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, kPipe>, wave_blocks(n, E), kCap, s, peers, P,
+        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe>, wave_blocks(n, E), kCap, s, peers, P,
                       n, group, cn, out_scale, out_codes, out_scales, out_f32);
     return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, false>, wave_blocks(n, E), kCap, s, peers, P, n,
                   group, cn, out_scale, out_codes, out_scales, out_f32);
