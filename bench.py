@@ -116,6 +116,7 @@ def main():
     ap.add_argument("--cpu-sample-log2", type=int, default=29)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--no-variants", action="store_true")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -201,6 +202,31 @@ def main():
         unfused = {"fused_gradient_ms": round(ue[0].elapsed_time(ue[1]) / 5, 4),
                    "unfused_gradient_ms": round(ue[2].elapsed_time(ue[3]) / 5, 4)}
 
+    # the paper's ablation variants on the same kernels and the same shard
+    variants = {}
+    if not args.no_variants:
+        def timed(fn, reps=5):
+            fn()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            return round(a.elapsed_time(b) / reps, 4)
+        for v in ("tlq_hs", "tlq", "ulq"):
+            variants[f"{v}_gradient_ms"] = timed(lambda: hp.gradient_variant(v))
+        g2 = 2048
+        codes = torch.empty(w.n // 2, dtype=torch.uint8, device="cuda")
+        sc = torch.empty(w.n // g2, device="cuda")
+        mn = torch.empty(w.n // g2, device="cuda")
+        variants["qwd_g2048_encode_ms"] = timed(lambda: sdp4.sdp4_qwd_encode(hp.w_new, hp.w_prev, g2, codes, sc, mn))
+        variants["qwd_g2048_decode_ms"] = timed(lambda: sdp4.sdp4_qwd_decode(codes, sc, mn, g2, hp.w_prev))
+        zero = torch.zeros(w.n, dtype=hp.w_prev.dtype, device="cuda")
+        variants["qw_g2048_encode_ms"] = timed(lambda: sdp4.sdp4_qwd_encode(hp.w_new, zero, g2, codes, sc, mn))
+        del codes, sc, mn, zero
+
     traffic = traffic_for(dom)
     line = {
         "metric": METRIC,
@@ -227,6 +253,8 @@ def main():
     }
     if unfused:
         line["hadamard_fusion"] = unfused
+    if variants:
+        line["variants"] = variants
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample ...")
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_log2, args.seed)

@@ -12,10 +12,10 @@ struct GradQuant {
                    hipStream_t s)
     {
         if (group > 64 * 32) {
-            auto k = bits == 8 ? k_grad_quant<8, 64, NB, kPipe> : k_grad_quant<4, 64, NB, kPipe>;
+            auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth> : k_grad_quant<4, 64, NB, kDepth>;
             return launch(k, wave_blocks(n, 64), kCap, s, x, n, group, cn, codes, scale);
         }
-        auto k = bits == 8 ? k_grad_quant<8, 32, NB, kPipe> : k_grad_quant<4, 32, NB, kPipe>;
+        auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth> : k_grad_quant<4, 32, NB, kDepth>;
         return launch(k, wave_blocks(n, 32), kCap, s, x, n, group, cn, codes, scale);
     }
 };
@@ -27,7 +27,7 @@ struct Hadamard {
         if constexpr (NB < 2)
             return 1;
         else
-            return launch(k_hadamard<32, NB, kPipe>, wave_blocks(n, 32), kCap, s, x, y, n, cn);
+            return launch(k_hadamard<32, NB, kDepth>, wave_blocks(n, 32), kCap, s, x, y, n, cn);
     }
 };
 

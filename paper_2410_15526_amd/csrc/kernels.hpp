@@ -16,7 +16,7 @@
 #include "launch.hpp"
 
 #ifndef SDP4_PIPE
-#define SDP4_PIPE 1
+#define SDP4_PIPE 1 // tiles prefetched ahead of the one being processed
 #endif
 #ifndef SDP4_PEER_LDS
 #define SDP4_PEER_LDS 1
@@ -27,36 +27,40 @@
 
 namespace sdp4 {
 
-constexpr bool kPipe = SDP4_PIPE != 0;
+constexpr int kDepth = SDP4_PIPE;
 
-template <bool PIPE, class Tile, class Load, class Proc>
+// Persistent loop of one wavefront over its tiles t, t + S, t + 2S, ...
+// (S = waves in the grid).  DEPTH = 0 loads and processes one tile at a
+// time; DEPTH = D >= 1 keeps the loads of the next D tiles in flight while
+// a tile is processed (a ring of D register buffers, indexed at compile
+// time by unrolling).
+template <int DEPTH, class Tile, class Load, class Proc>
 SDP4_DEV void tile_loop(int64_t ntiles, Load load, Proc proc)
 {
     const int wave = threadIdx.x / kWave;
     const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
     int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave;
-    if constexpr (!PIPE) {
+    if constexpr (DEPTH == 0) {
         for (; t < ntiles; t += stride) {
             Tile in;
             load(t, in);
             proc(t, in);
         }
     } else {
-        if (t >= ntiles)
-            return;
-        Tile cur;
-        load(t, cur);
+        Tile buf[DEPTH];
+#pragma unroll
+        for (int k = 0; k < DEPTH; ++k)
+            if (t + k * stride < ntiles)
+                load(t + k * stride, buf[k]);
         for (;;) {
-            const int64_t tn = t + stride;
-            if (tn < ntiles) {
-                Tile nxt;
-                load(tn, nxt);
-                proc(t, cur);
-                cur = nxt;
-                t = tn;
-            } else {
-                proc(t, cur);
-                break;
+#pragma unroll
+            for (int k = 0; k < DEPTH; ++k) {
+                if (t >= ntiles)
+                    return;
+                proc(t, buf[k]);
+                if (t + DEPTH * stride < ntiles)
+                    load(t + DEPTH * stride, buf[k]);
+                t += stride;
             }
         }
     }
@@ -94,7 +98,7 @@ SDP4_DEV void maybe_fwht(float (&v)[E], float cn)
 // ---------------------------------------------------------------------------
 // qWD encode: d = w_new - widen(w_prev); asymmetric 4-bit codes per group
 // ---------------------------------------------------------------------------
-template <bool BF16, int E, bool PIPE>
+template <bool BF16, int E, int DEPTH>
 __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
     const float *__restrict__ w_new, const void *__restrict__ w_prev, int64_t n, int group,
     uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv)
@@ -165,13 +169,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
             minv[gi] = mn;
         }
     };
-    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
 // qWD decode: w_prev <- narrow(widen(w_prev) + fma(code, scale, min))
 // ---------------------------------------------------------------------------
-template <bool BF16, int E, bool PIPE>
+template <bool BF16, int E, int DEPTH>
 __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const float *__restrict__ minv, int64_t n, int group, void *__restrict__ w_prev)
@@ -236,13 +240,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
             stage_out<RP>(reinterpret_cast<u32x4 *>(static_cast<float *>(w_prev) + base), valid / 4, lds, c);
         }
     };
-    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
 // K1: blockwise Hadamard (block NB, 0 = none) + symmetric BITS-bit group quantization
 // ---------------------------------------------------------------------------
-template <int BITS, int E, int NB, bool PIPE>
+template <int BITS, int E, int NB, int DEPTH>
 __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
     const float *__restrict__ x, int64_t n, int group, float cn, uint8_t *__restrict__ codes,
     float *__restrict__ scale)
@@ -287,7 +291,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
         if (off < valid && off % group == 0)
             scale[(base + off) / group] = s;
     };
-    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
@@ -295,7 +299,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
 // (BITS_OUT 4/8) or inverse Hadamard (block NB) + out_scale to float32
 // (BITS_OUT 0)
 // ---------------------------------------------------------------------------
-template <int BITS_IN, int BITS_OUT, int E, int NB, int PMAX, bool PIPE>
+template <int BITS_IN, int BITS_OUT, int E, int NB, int PMAX, int DEPTH>
 __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
     PeerTable peers, int P, int64_t n, int group, float cn, float out_scale, uint8_t *__restrict__ out_codes,
     float *__restrict__ out_scales, float *__restrict__ out_f32)
@@ -405,13 +409,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
                 out_scales[(base + off) / group] = s;
         }
     };
-    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
 // standalone Hadamard (unfused variant); in place allowed
 // ---------------------------------------------------------------------------
-template <int E, int NB, bool PIPE>
+template <int E, int NB, int DEPTH>
 __global__ __launch_bounds__(kBlockThreads) void k_hadamard(const float *x, float *y, int64_t n, float cn)
 {
     constexpr int W = kWave * E;
@@ -437,7 +441,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_hadamard(const float *x, floa
         f32_to_chunks<E>(v, c);
         stage_out<R>(reinterpret_cast<u32x4 *>(y + base), tile_valid(n, base, W) / 4, lds, c);
     };
-    tile_loop<PIPE, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
@@ -482,14 +486,14 @@ template <int BITS_IN, int BITS_OUT, int E, int NB>
 int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, float out_scale,
               uint8_t *out_codes, float *out_scales, float *out_f32, hipStream_t s)
 {
-    constexpr bool pipe = kPipe && BITS_OUT == 0;
+    constexpr int pipe = BITS_OUT == 0 ? kDepth : 0;
     if (P <= 4)
         return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe>, wave_blocks(n, E), kCap, s, peers, P,
                       n, group, cn, out_scale, out_codes, out_scales, out_f32);
     if (P <= 8)
         return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe>, wave_blocks(n, E), kCap, s, peers, P,
                       n, group, cn, out_scale, out_codes, out_scales, out_f32);
-    return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, false>, wave_blocks(n, E), kCap, s, peers, P, n,
+    return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, 0>, wave_blocks(n, E), kCap, s, peers, P, n,
                   group, cn, out_scale, out_codes, out_scales, out_f32);
 }
 

@@ -64,12 +64,14 @@ class HotPath:
     def qwd_decode(self, stream=None):
         sdp4.sdp4_qwd_decode(self.qcodes, self.qscale, self.qmin, self.qwd_group, self.w_prev, stream=stream)
 
-    def grad_quant(self, stream=None):
-        sdp4.sdp4_grad_quant(self.grad, 8, self.block, self.group, self.c8, self.s8, stream=stream)
+    def grad_quant(self, stream=None, bits=8, block=None):
+        block = self.block if block is None else block
+        sdp4.sdp4_grad_quant(self.grad, bits, block, self.group, self.c8, self.s8, stream=stream)
 
-    def intra_chunks(self):
+    def intra_chunks(self, bits=8):
         M, g = self.M, self.group
-        return ([self.c8[p * M:(p + 1) * M] for p in range(self.P)],
+        cb = M * bits // 8
+        return ([self.c8[p * cb:(p + 1) * cb] for p in range(self.P)],
                 [self.s8[p * M // g:(p + 1) * M // g] for p in range(self.P)])
 
     def inter_chunks(self):
@@ -77,14 +79,24 @@ class HotPath:
         return ([self.c4[q * m // 2:(q + 1) * m // 2] for q in range(self.Q)],
                 [self.s4[q * m // g:(q + 1) * m // g] for q in range(self.Q)])
 
-    def reduce_intra(self, stream=None):
-        c, s = self.intra_chunks()
-        sdp4.sdp4_dequant_reduce(c, s, self.M, 8, self.group, 4, 0, 1.0, self.c4, self.s4, None, stream=stream)
+    def reduce_intra(self, stream=None, bits_in=8):
+        c, s = self.intra_chunks(bits_in)
+        sdp4.sdp4_dequant_reduce(c, s, self.M, bits_in, self.group, 4, 0, 1.0, self.c4, self.s4, None,
+                                 stream=stream)
 
-    def reduce_inter(self, stream=None):
+    def reduce_inter(self, stream=None, block=None):
+        block = self.block if block is None else block
         c, s = self.inter_chunks()
-        sdp4.sdp4_dequant_reduce(c, s, self.m, 4, self.group, 0, self.block, self.out_scale, None, None,
+        sdp4.sdp4_dequant_reduce(c, s, self.m, 4, self.group, 0, block, self.out_scale, None, None,
                                  self.out, stream=stream)
+
+    def gradient_variant(self, name: str, stream=None):
+        """The paper's gradient strategies (Sec. 5.1, Sec. 5.4) on the same kernels:
+        TLq-HS (8-bit then 4-bit, Hadamard), TLq (no Hadamard), ULq (4-bit twice, no Hadamard)."""
+        bits1, block = {"tlq_hs": (8, self.block), "tlq": (8, 0), "ulq": (4, 0)}[name]
+        self.grad_quant(stream, bits=bits1, block=block)
+        self.reduce_intra(stream, bits_in=bits1)
+        self.reduce_inter(stream, block=block)
 
     def launches(self):
         return [("qwd_encode", self.qwd_encode), ("qwd_decode", self.qwd_decode),

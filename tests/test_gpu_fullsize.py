@@ -53,34 +53,35 @@ def check_qwd(hp, w, seed, starts, L):
         assert np.array_equal(got.view(np.uint8), np.ascontiguousarray(want).view(np.uint8)), f"decode@{a}"
 
 
-def k1_ref(w, seed, a, L):
+def k1_ref(w, seed, a, L, bits=8, block=None):
     x = synth.gradient(w, a, L, seed)
-    return oracle.grad_quant(x, 8, w.hadamard_block, w.group)
+    return oracle.grad_quant(x, bits, w.hadamard_block if block is None else block, w.group)
 
 
-def k2_ref(w, seed, x, L):
+def k2_ref(w, seed, x, L, bits=8, block=None):
     """Oracle K2 output segment [x, x+L) of the intra-node reduction."""
     M, g = w.n // w.P, w.group
-    k1 = [k1_ref(w, seed, p * M + x, L) for p in range(w.P)]
-    return oracle.dequant_reduce([c for c, _, _ in k1], [s for _, s, _ in k1], L, 8, g, 4, want_f32=False)
+    k1 = [k1_ref(w, seed, p * M + x, L, bits, block) for p in range(w.P)]
+    return oracle.dequant_reduce([c for c, _, _ in k1], [s for _, s, _ in k1], L, bits, g, 4, want_f32=False)
 
 
-def check_gradient_path(hp, w, seed, starts_k1, starts_k3, L):
+def check_gradient_path(hp, w, seed, starts_k1, starts_k3, L, bits=8, block=None):
+    block = w.hadamard_block if block is None else block
     g, M, m = w.group, w.n // w.P, w.n // w.P // w.Q
     for a in starts_k1:
-        rc, rs, pre = k1_ref(w, seed, a, L)
-        check_codes(host(hp.c8[a:a + L]), rc, pre, L, 8, what=f"k1@{a}")
+        rc, rs, pre = k1_ref(w, seed, a, L, bits, block)
+        check_codes(host(hp.c8[a * bits // 8:(a + L) * bits // 8]), rc, pre, L, bits, what=f"k1@{a}")
         check_headers(host(hp.s8[a // g:(a + L) // g]), rs, f"k1 scale@{a}")
     for a in starts_k3:
         parts = []
         for q in range(w.Q):
-            r = k2_ref(w, seed, q * m + a, L)
+            r = k2_ref(w, seed, q * m + a, L, bits, block)
             x = q * m + a
             check_codes(host(hp.c4[x // 2:(x + L) // 2]), r["codes"], r["pre"], L, 4, what=f"k2@{x}")
             check_headers(host(hp.s4[x // g:(x + L) // g]), r["scales"], f"k2 scale@{x}")
             parts.append(r)
         want = oracle.dequant_reduce([r["codes"] for r in parts], [r["scales"] for r in parts], L, 4, g, 0,
-                                     w.hadamard_block, 1.0 / (w.P * w.Q))["f32"]
+                                     block, 1.0 / (w.P * w.Q))["f32"]
         check_f32(host(hp.out[a:a + L]), want, f"k3@{a}")
 
 
@@ -143,6 +144,21 @@ def test_full_shard_step(name):
             rc, rs, rm, pre = oracle.qwd_encode(synth.new_weights(w, a, Lq, seed), prev, g)
             check_codes(host(hp.qcodes[a // 2:(a + Lq) // 2]), rc, pre, Lq, 4, signed=False)
             check_f32(host(prev32[a:a + Lq]), oracle.qwd_decode(rc, rs, rm, prev, g))
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("variant,bits,block", [("tlq", 8, 0), ("ulq", 4, 0)])
+def test_paper_variants_full_shard(variant, bits, block):
+    """TLq (no Hadamard) and ULq (4-bit twice, no Hadamard) of Sec. 5.1 / 5.4 on
+    the GPT-1.3B shard, through the same launch sequence as the benchmark."""
+    w = synth.WORKLOADS["c3"]
+    hp = build(w, 0)
+    say(f"c3 variant {variant}")
+    hp.gradient_variant(variant)
+    torch().cuda.synchronize()
+    L = 4 * w.group
+    check_gradient_path(hp, w, 0, segments(w.n, L, 8, 5), segments(w.n // w.P // w.Q, L, 4, 6), L,
+                        bits=bits, block=block)
 
 
 def test_tiny_shard_step_every_element():
