@@ -215,7 +215,7 @@ def main():
             b.record()
             torch.cuda.synchronize()
             return round(a.elapsed_time(b) / reps, 4)
-        for v in ("tlq_hs", "tlq", "ulq"):
+        for v in ("tlq_hs", "tlq", "ulq", "tlq_hs_sr"):
             variants[f"{v}_gradient_ms"] = timed(lambda: hp.gradient_variant(v))
         g2 = 2048
         codes = torch.empty(w.n // 2, dtype=torch.uint8, device="cuda")

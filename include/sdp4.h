@@ -182,6 +182,34 @@ int sdp4_dequant_reduce(int P, const void *const *codes, const float *const *sca
                         void *stream);
 
 /*
+ * Stochastically rounded variants of the two gradient quantizers.  The
+ * convergence analysis (Sec. 4.2: U_g in Alg. 3 is an unbiased compressor,
+ * Definition of the unbiased kappa-approximate compressor) assumes unbiased
+ * gradient compression; with stochastic rounding the symmetric quantizer is
+ * unbiased: code = clamp(floor(fl(x * inv) + u), -qmax, qmax) with
+ * u in [0, 1) drawn per element, so E[code * scale] = x (up to 2^-16 of a
+ * quantization step).
+ *
+ * u of element e = offset + i (i the index within this call) is the 16-bit
+ * uniform u = h / 65536, h = half (e % 2: 0 low, 1 high) of word (e / 2) % 4
+ * of Philox4x32-10 (Salmon et al., SC'11) with counter (e / 8 as two 32-bit
+ * words low first, 0, 0) and key (seed low word, seed high word).  The same
+ * (seed, e) always gives the same u, so a buffer quantized in pieces with
+ * matching offsets equals the one-call result.
+ *
+ *   seed     64-bit key of the generator (e.g. derived from the step and rank)
+ *   offset   element position of x[0] in the caller's stream; multiple of 8
+ * Other arguments, layouts and errors as sdp4_grad_quant / the bits_out > 0
+ * mode of sdp4_dequant_reduce (bits_out must be 4 or 8; there is no
+ * transform in this mode).  offset not a multiple of 8: EALIGN.
+ */
+int sdp4_grad_quant_sr(const float *x, int64_t n, int bits, int hadamard_block, int group, uint64_t seed,
+                       uint64_t offset, void *codes, float *scale, void *stream);
+int sdp4_dequant_reduce_sr(int P, const void *const *codes, const float *const *scales, int64_t n_chunk,
+                           int bits_in, int group, int bits_out, uint64_t seed, uint64_t offset,
+                           void *out_codes, float *out_scales, float *out_f32, void *stream);
+
+/*
  * Standalone blockwise Hadamard transform (the unfused "HS w/o fused"
  * variant of Table 4, Sec. 5.4): y = (H_n / sqrt(n)) x per block.
  *   x, y [n] float32   y == x (in place) is allowed; partial overlap is not

@@ -66,6 +66,12 @@ def lib() -> C.CDLL:
                 "sdp4ref_hadamard": (i32, [vp, vp, i64, i32]),
                 "sdp4ref_reduce_f32": (i32, [i32, vp, vp, i64]),
                 "sdp4ref_version": (C.c_char_p, []),
+                "sdp4ref_philox4x32_10": (None, [vp, vp, vp]),
+                "sdp4ref_sr_uniform": (f32, [C.c_uint64, C.c_uint64]),
+                "sdp4ref_quant_sym_sr": (i32, [vp, i64, i32, i32, C.c_uint64, C.c_uint64, vp, vp, vp]),
+                "sdp4ref_grad_quant_sr": (i32, [vp, i64, i32, i32, i32, C.c_uint64, C.c_uint64, vp, vp, vp]),
+                "sdp4ref_dequant_reduce_sr": (i32, [i32, vp, vp, i64, i32, i32, i32, C.c_uint64, C.c_uint64,
+                                                    vp, vp, vp, vp]),
             }
             for name, (res, args) in sig.items():
                 fn = getattr(L, name)
@@ -259,3 +265,57 @@ def reduce_f32(xs) -> np.ndarray:
     y = np.empty(n, np.float32)
     _ck(lib().sdp4ref_reduce_f32(len(xs), C.cast(ptr, C.c_void_p), _p(y), n), "reduce_f32")
     return y
+
+
+# --------------------------------------------------------------------------
+# stochastic rounding (counter-based Philox4x32-10 random numbers)
+# --------------------------------------------------------------------------
+
+def philox4x32_10(ctr, key) -> np.ndarray:
+    c = np.ascontiguousarray(ctr, np.uint32)
+    k = np.ascontiguousarray(key, np.uint32)
+    out = np.empty(4, np.uint32)
+    lib().sdp4ref_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def sr_uniform(seed: int, e: int) -> float:
+    return float(lib().sdp4ref_sr_uniform(seed, e))
+
+
+def quant_sym_sr(x, group: int, bits: int, seed: int, offset: int = 0):
+    x = _f32(x)
+    q = np.empty(x.size, np.int8)
+    s = np.empty(x.size // group, np.float32)
+    pre = np.empty(x.size, np.float32)
+    _ck(lib().sdp4ref_quant_sym_sr(_p(x), x.size, group, bits, seed, offset, _p(q), _p(s), _p(pre)),
+        "quant_sym_sr")
+    return q, s, pre
+
+
+def grad_quant_sr(x, bits: int, hadamard_block: int, group: int, seed: int, offset: int = 0):
+    x = _f32(x)
+    n = x.size
+    codes = np.empty(n, np.int8) if bits == 8 else np.empty(n // 2, np.uint8)
+    s = np.empty(n // group, np.float32)
+    pre = np.empty(n, np.float32)
+    _ck(lib().sdp4ref_grad_quant_sr(_p(x), n, bits, hadamard_block, group, seed, offset, _p(codes), _p(s),
+                                    _p(pre)), "grad_quant_sr")
+    return codes, s, pre
+
+
+def dequant_reduce_sr(codes_list, scales_list, n_chunk: int, bits_in: int, group: int, bits_out: int,
+                      seed: int, offset: int = 0, want_f32: bool = True):
+    P = len(codes_list)
+    cl = [np.ascontiguousarray(c) for c in codes_list]
+    sl = [_f32(s) for s in scales_list]
+    cptr = (C.c_void_p * P)(*[c.ctypes.data for c in cl])
+    sptr = (C.c_void_p * P)(*[s.ctypes.data for s in sl])
+    oc = np.empty(n_chunk, np.int8) if bits_out == 8 else np.empty(n_chunk // 2, np.uint8)
+    os_ = np.empty(n_chunk // group, np.float32)
+    pre = np.empty(n_chunk, np.float32)
+    f = np.empty(n_chunk, np.float32) if want_f32 else None
+    _ck(lib().sdp4ref_dequant_reduce_sr(P, C.cast(cptr, C.c_void_p), C.cast(sptr, C.c_void_p), n_chunk, bits_in,
+                                        group, bits_out, seed, offset, _p(oc), _p(os_), _p(f), _p(pre)),
+        "dequant_reduce_sr")
+    return dict(codes=oc, scales=os_, f32=f, pre=pre)

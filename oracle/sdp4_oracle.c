@@ -471,3 +471,176 @@ int sdp4ref_reduce_f32(int P, const float *const *xs, float *y, int64_t n)
     }
     return REF_OK;
 }
+
+/* ------------------------------------------------------------------------
+ * Stochastic rounding for the gradient quantizers.  The convergence
+ * analysis (Sec. 4.2, the compressor U_g of Alg. 3 and Definition
+ * "unbiased kappa-approximate compressor") assumes an unbiased gradient
+ * compressor; rounding the scaled value v up with probability frac(v) makes
+ * the symmetric quantizer unbiased.
+ *
+ * The random numbers come from the counter-based generator Philox4x32 with
+ * 10 rounds (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy
+ * as 1, 2, 3", SC'11), keyed by a 64-bit seed and indexed by the element
+ * position e = offset + i:
+ *   counter = (e / 8 low word, e / 8 high word, 0, 0), key = (seed low, seed high),
+ *   word    = output[(e / 2) % 4],
+ *   u       = (e even ? low half : high half of word) / 65536        in [0, 1),
+ *   code    = clamp(floor(fl(fl(x * inv) + u)), -qmax, qmax).
+ * ---------------------------------------------------------------------- */
+
+/* One Philox4x32 round: two 32x32->64 products, the halves mixed with the
+ * other two counter words and the key. */
+static void philox_round(uint32_t c[4], const uint32_t k[2])
+{
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c[0];
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c[2];
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k[0];
+    const uint32_t n1 = (uint32_t)p1;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k[1];
+    const uint32_t n3 = (uint32_t)p0;
+    c[0] = n0;
+    c[1] = n1;
+    c[2] = n2;
+    c[3] = n3;
+}
+
+void sdp4ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c[4] = {ctr[0], ctr[1], ctr[2], ctr[3]};
+    uint32_t k[2] = {key[0], key[1]};
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) { /* key schedule: add the Weyl constants between rounds */
+            k[0] += 0x9E3779B9u;
+            k[1] += 0xBB67AE85u;
+        }
+        philox_round(c, k);
+    }
+    for (int i = 0; i < 4; ++i)
+        out[i] = c[i];
+}
+
+float sdp4ref_sr_uniform(uint64_t seed, uint64_t e)
+{
+    const uint64_t blk = e / 8;
+    const uint32_t ctr[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), 0u, 0u};
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t out[4];
+    sdp4ref_philox4x32_10(ctr, key, out);
+    const uint32_t word = out[(e / 2) % 4];
+    const uint32_t half = (e % 2) ? (word >> 16) : (word & 0xFFFFu);
+    return (float)half / 65536.0f;
+}
+
+int sdp4ref_quant_sym_sr(const float *x, int64_t n, int group, int bits, uint64_t seed,
+                         uint64_t offset, int8_t *q, float *scale, float *pre)
+{
+    if (!x || !q || !scale || group < 1 || n % group || bits < 2 || bits > 8)
+        return REF_EINVAL;
+    if (!all_finite(x, n))
+        return REF_ENONFINITE;
+    const float qmax = (float)((1 << (bits - 1)) - 1);
+    for (int64_t g0 = 0, gi = 0; g0 < n; g0 += group, ++gi) {
+        float s = 0.0f;
+        for (int i = 0; i < group; ++i) {
+            float m = fabsf(x[g0 + i]);
+            if (m > s)
+                s = m;
+        }
+        float inv = qmax / s;
+        if (s == 0.0f || !isfinite(inv)) {
+            scale[gi] = 0.0f;
+            for (int i = 0; i < group; ++i) {
+                q[g0 + i] = 0;
+                if (pre)
+                    pre[g0 + i] = 0.0f;
+            }
+            continue;
+        }
+        scale[gi] = s / qmax;
+        for (int i = 0; i < group; ++i) {
+            float v = x[g0 + i] * inv;
+            if (pre)
+                pre[g0 + i] = v;
+            float u = sdp4ref_sr_uniform(seed, offset + (uint64_t)(g0 + i));
+            float r = floorf(v + u);
+            if (r > qmax)
+                r = qmax;
+            if (r < -qmax)
+                r = -qmax;
+            q[g0 + i] = (int8_t)r;
+        }
+    }
+    return REF_OK;
+}
+
+/* grad_quant with stochastic rounding: transform (if any), then the
+ * stochastically rounded symmetric quantizer; same layouts as grad_quant. */
+int sdp4ref_grad_quant_sr(const float *x, int64_t n, int bits, int hadamard_block, int group,
+                          uint64_t seed, uint64_t offset, void *codes, float *scale, float *pre)
+{
+    if (!x || !codes || !scale || !codes_ok(bits) || group < 2 || n % group || offset % 8)
+        return REF_EINVAL;
+    if (hadamard_block && (n % hadamard_block || !is_pow2(hadamard_block) || hadamard_block < 2))
+        return REF_EINVAL;
+    float *y = malloc(sizeof(float) * (size_t)(n ? n : 1));
+    int8_t *q = malloc((size_t)(n ? n : 1));
+    if (!y || !q) {
+        free(y);
+        free(q);
+        return REF_EINVAL;
+    }
+    memcpy(y, x, sizeof(float) * (size_t)n);
+    int rc = hadamard_block ? sdp4ref_fwht(y, n, hadamard_block) : REF_OK;
+    if (rc == REF_OK)
+        rc = sdp4ref_quant_sym_sr(y, n, group, bits, seed, offset, q, scale, pre);
+    if (rc == REF_OK) {
+        if (bits == 8)
+            memcpy(codes, q, (size_t)n);
+        else
+            rc = sdp4ref_pack4(q, n, (uint8_t *)codes);
+    }
+    free(y);
+    free(q);
+    return rc;
+}
+
+/* dequantize-reduce with stochastically rounded re-quantization (bits_out
+ * 4 or 8; no transform): the same reduction as sdp4ref_dequant_reduce. */
+int sdp4ref_dequant_reduce_sr(int P, const void *const *codes, const float *const *scales,
+                              int64_t n_chunk, int bits_in, int group, int bits_out, uint64_t seed,
+                              uint64_t offset, void *out_codes, float *out_scales, float *out_f32,
+                              float *pre)
+{
+    if (P < 1 || !codes || !scales || !codes_ok(bits_in) || !codes_ok(bits_out) || group < 2 ||
+        n_chunk % group || !out_codes || !out_scales || offset % 8)
+        return REF_EINVAL;
+    for (int p = 0; p < P; ++p)
+        if (!codes[p] || !scales[p])
+            return REF_EINVAL;
+    float *r = malloc(sizeof(float) * (size_t)(n_chunk ? n_chunk : 1));
+    int8_t *q = malloc((size_t)(n_chunk ? n_chunk : 1));
+    if (!r || !q) {
+        free(r);
+        free(q);
+        return REF_EINVAL;
+    }
+    for (int64_t i = 0; i < n_chunk; ++i) {
+        float acc = 0.0f;
+        for (int p = 0; p < P; ++p)
+            acc = fmaf((float)code_at(codes[p], i, bits_in), scales[p][i / group], acc);
+        r[i] = acc;
+    }
+    if (out_f32)
+        memcpy(out_f32, r, sizeof(float) * (size_t)n_chunk);
+    int rc = sdp4ref_quant_sym_sr(r, n_chunk, group, bits_out, seed, offset, q, out_scales, pre);
+    if (rc == REF_OK) {
+        if (bits_out == 8)
+            memcpy(out_codes, q, (size_t)n_chunk);
+        else
+            rc = sdp4ref_pack4(q, n_chunk, (uint8_t *)out_codes);
+    }
+    free(r);
+    free(q);
+    return rc;
+}

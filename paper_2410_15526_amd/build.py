@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsdp4.so")
-SOURCES = ["k_qwd.hip", "k_grad.hip", "k_reduce.hip", "k_reduce_f32_in8.hip", "k_reduce_f32_in4.hip",
+SOURCES = ["k_qwd.hip", "k_grad.hip", "k_sr.hip", "k_reduce.hip", "k_reduce_f32_in8.hip", "k_reduce_f32_in4.hip",
            "launch.cpp", "abi.cpp"]
 ARCH = "gfx950"
 

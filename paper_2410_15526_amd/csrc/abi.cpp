@@ -53,6 +53,45 @@ float hadamard_scale(int n) { return n > 1 ? static_cast<float>(1.0 / std::sqrt(
 
 hipStream_t as_stream(void *s) { return static_cast<hipStream_t>(s); }
 
+// Pointer checks shared by the dequantize-reduce entry points: non-null,
+// aligned, outputs overlapping neither an input chunk nor each other.
+int check_reduce_args(int P, const void *const *codes, const float *const *scales, int64_t n_chunk, int bits_in,
+                      int group, int bits_out, void *out_codes, float *out_scales, float *out_f32,
+                      PeerTable &peers)
+{
+    if (!codes || !scales)
+        return SDP4_EINVAL;
+    if (bits_out ? (!out_codes || !out_scales) : !out_f32)
+        return SDP4_EINVAL;
+    const int64_t ng = n_chunk / group;
+    const int64_t in_cb = n_chunk * bits_in / 8;
+    const int64_t out_cb = n_chunk * bits_out / 8;
+    for (int p = 0; p < P; ++p) {
+        if (!codes[p] || !scales[p])
+            return SDP4_EINVAL;
+        if (!aligned(codes[p], 16) || !aligned(scales[p], 4))
+            return SDP4_EALIGN;
+        peers.codes[p] = codes[p];
+        peers.scales[p] = scales[p];
+    }
+    if ((out_codes && !aligned(out_codes, 16)) || (out_scales && !aligned(out_scales, 4)) ||
+        (out_f32 && !aligned(out_f32, 16)))
+        return SDP4_EALIGN;
+    const void *outs[3] = {bits_out ? out_codes : nullptr, bits_out ? out_scales : nullptr, out_f32};
+    const int64_t outn[3] = {bits_out ? out_cb : 0, bits_out ? 4 * ng : 0, out_f32 ? 4 * n_chunk : 0};
+    for (int i = 0; i < 3; ++i) {
+        if (!outs[i])
+            continue;
+        for (int p = 0; p < P; ++p)
+            if (overlap(outs[i], outn[i], codes[p], in_cb) || overlap(outs[i], outn[i], scales[p], 4 * ng))
+                return SDP4_EINVAL;
+        for (int j = 0; j < i; ++j)
+            if (outs[j] && overlap(outs[i], outn[i], outs[j], outn[j]))
+                return SDP4_EINVAL;
+    }
+    return SDP4_OK;
+}
+
 } // namespace
 
 extern "C" {
@@ -128,6 +167,48 @@ int sdp4_grad_quant(const float *x, int64_t n, int bits, int hadamard_block, int
                                    static_cast<uint8_t *>(codes), scale, as_stream(stream));
 }
 
+int sdp4_grad_quant_sr(const float *x, int64_t n, int bits, int hadamard_block, int group, uint64_t seed,
+                       uint64_t offset, void *codes, float *scale, void *stream)
+{
+    if (n < 0 || !valid_bits(bits) || !valid_block(hadamard_block) || !valid_group(group))
+        return SDP4_EINVAL;
+    if (n % lcm_pow2(group, hadamard_block) || offset % 8)
+        return SDP4_EALIGN;
+    if (n == 0)
+        return SDP4_OK;
+    if (!x || !codes || !scale)
+        return SDP4_EINVAL;
+    if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scale, 4))
+        return SDP4_EALIGN;
+    const int64_t cb = n * bits / 8, sb = 4 * (n / group);
+    if (overlap(codes, cb, x, 4 * n) || overlap(scale, sb, x, 4 * n) || overlap(codes, cb, scale, sb))
+        return SDP4_EINVAL;
+    return sdp4::launch_grad_quant_sr(x, n, bits, hadamard_block, group, hadamard_scale(hadamard_block), seed,
+                                      offset, static_cast<uint8_t *>(codes), scale, as_stream(stream));
+}
+
+int sdp4_dequant_reduce_sr(int P, const void *const *codes, const float *const *scales, int64_t n_chunk,
+                           int bits_in, int group, int bits_out, uint64_t seed, uint64_t offset,
+                           void *out_codes, float *out_scales, float *out_f32, void *stream)
+{
+    if (P < 1 || P > SDP4_MAX_PEERS)
+        return SDP4_ERANGE;
+    if (n_chunk < 0 || !valid_bits(bits_in) || !valid_group(group) || !valid_bits(bits_out))
+        return SDP4_EINVAL;
+    if (n_chunk % group || offset % 8)
+        return SDP4_EALIGN;
+    if (n_chunk == 0)
+        return SDP4_OK;
+    PeerTable peers{};
+    const int rc = check_reduce_args(P, codes, scales, n_chunk, bits_in, group, bits_out, out_codes, out_scales,
+                                     out_f32, peers);
+    if (rc != SDP4_OK)
+        return rc;
+    return sdp4::launch_dequant_reduce_sr(peers, P, n_chunk, bits_in, group, bits_out, seed, offset,
+                                          static_cast<uint8_t *>(out_codes), out_scales, out_f32,
+                                          as_stream(stream));
+}
+
 int sdp4_dequant_reduce(int P, const void *const *codes, const float *const *scales,
                         int64_t n_chunk, int bits_in, int group, int bits_out, int hadamard_block,
                         float out_scale, void *out_codes, float *out_scales, float *out_f32,
@@ -144,37 +225,11 @@ int sdp4_dequant_reduce(int P, const void *const *codes, const float *const *sca
         return SDP4_EALIGN;
     if (n_chunk == 0)
         return SDP4_OK;
-    if (!codes || !scales)
-        return SDP4_EINVAL;
-    if (bits_out ? (!out_codes || !out_scales) : !out_f32)
-        return SDP4_EINVAL;
-    const int64_t ng = n_chunk / group;
-    const int64_t in_cb = n_chunk * bits_in / 8;
-    const int64_t out_cb = n_chunk * bits_out / 8;
     PeerTable peers{};
-    for (int p = 0; p < P; ++p) {
-        if (!codes[p] || !scales[p])
-            return SDP4_EINVAL;
-        if (!aligned(codes[p], 16) || !aligned(scales[p], 4))
-            return SDP4_EALIGN;
-        peers.codes[p] = codes[p];
-        peers.scales[p] = scales[p];
-    }
-    if ((out_codes && !aligned(out_codes, 16)) || (out_scales && !aligned(out_scales, 4)) ||
-        (out_f32 && !aligned(out_f32, 16)))
-        return SDP4_EALIGN;
-    const void *outs[3] = {bits_out ? out_codes : nullptr, bits_out ? out_scales : nullptr, out_f32};
-    const int64_t outn[3] = {bits_out ? out_cb : 0, bits_out ? 4 * ng : 0, out_f32 ? 4 * n_chunk : 0};
-    for (int i = 0; i < 3; ++i) {
-        if (!outs[i])
-            continue;
-        for (int p = 0; p < P; ++p)
-            if (overlap(outs[i], outn[i], codes[p], in_cb) || overlap(outs[i], outn[i], scales[p], 4 * ng))
-                return SDP4_EINVAL;
-        for (int j = 0; j < i; ++j)
-            if (outs[j] && overlap(outs[i], outn[i], outs[j], outn[j]))
-                return SDP4_EINVAL;
-    }
+    const int rc = check_reduce_args(P, codes, scales, n_chunk, bits_in, group, bits_out, out_codes, out_scales,
+                                     out_f32, peers);
+    if (rc != SDP4_OK)
+        return rc;
     return sdp4::launch_dequant_reduce(peers, P, n_chunk, bits_in, group, bits_out, hadamard_block,
                                        hadamard_scale(hadamard_block), out_scale,
                                        static_cast<uint8_t *>(bits_out ? out_codes : nullptr),

@@ -321,6 +321,59 @@ SDP4_DEV void pack4(const uint32_t (&t)[E], u32x4 (&c)[E / 32])
     }
 }
 
+// ---------------------------------------------------------------------------
+// stochastic rounding: counter-based Philox4x32 with 10 rounds (Salmon,
+// Moraes, Dror, Shaw, SC'11) keyed by a 64-bit seed
+// ---------------------------------------------------------------------------
+SDP4_DEV void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c[0];
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c[2];
+        const uint32_t x0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0;
+        const uint32_t x2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+        c[1] = (uint32_t)p1;
+        c[3] = (uint32_t)p0;
+        c[0] = x0;
+        c[2] = x2;
+    }
+}
+
+// 16-bit uniforms u[i] in [0, 1) of elements e0 .. e0 + E - 1 (e0 a multiple
+// of 8): block e / 8 of the generator gives 8 elements, element e takes half
+// (e % 2) of word (e / 2) % 4.
+template <int E>
+SDP4_DEV void sr_uniforms(uint64_t seed, uint64_t e0, float (&u)[E])
+{
+    static_assert(E % 8 == 0, "lane slice");
+#pragma unroll
+    for (int j = 0; j < E / 8; ++j) {
+        const uint64_t blk = e0 / 8 + j;
+        uint32_t c[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), 0u, 0u};
+        philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            u[8 * j + 2 * w] = (float)(c[w] & 0xFFFFu) * (1.0f / 65536.0f);
+            u[8 * j + 2 * w + 1] = (float)(c[w] >> 16) * (1.0f / 65536.0f);
+        }
+    }
+}
+
+// Stochastically rounded code bits: floor(fl(fl(x * inv) + u)) clamped to
+// [-qmax, qmax] (fl(x * inv) may exceed qmax by an ulp, so the floor of the
+// sum can reach qmax + 1), returned like code_bits.
+SDP4_DEV uint32_t code_bits_sr(float x, float inv, float u, float qmax)
+{
+    const float v = x * inv;
+    const float f = __builtin_amdgcn_fmed3f(__builtin_floorf(v + u), -qmax, qmax);
+    return __float_as_uint(f + kRoundMagic);
+}
+
 // signed code e of a chunk array holding `bits`-wide codes
 template <int BITS>
 SDP4_DEV float code_f(const uint32_t *w, int e)

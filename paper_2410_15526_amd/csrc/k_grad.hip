@@ -13,10 +13,10 @@ struct GradQuant {
     {
         if (group > 64 * 32) {
             auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth> : k_grad_quant<4, 64, NB, kDepth>;
-            return launch(k, wave_blocks(n, 64), kCap, s, x, n, group, cn, codes, scale);
+            return launch(k, wave_blocks(n, 64), kCap, s, x, n, group, cn, codes, scale, uint64_t(0), uint64_t(0));
         }
         auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth> : k_grad_quant<4, 32, NB, kDepth>;
-        return launch(k, wave_blocks(n, 32), kCap, s, x, n, group, cn, codes, scale);
+        return launch(k, wave_blocks(n, 32), kCap, s, x, n, group, cn, codes, scale, uint64_t(0), uint64_t(0));
     }
 };
 

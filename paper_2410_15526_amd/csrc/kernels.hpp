@@ -246,10 +246,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
 // ---------------------------------------------------------------------------
 // K1: blockwise Hadamard (block NB, 0 = none) + symmetric BITS-bit group quantization
 // ---------------------------------------------------------------------------
-template <int BITS, int E, int NB, int DEPTH>
+template <int BITS, int E, int NB, int DEPTH, bool SR = false>
 __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
     const float *__restrict__ x, int64_t n, int group, float cn, uint8_t *__restrict__ codes,
-    float *__restrict__ scale)
+    float *__restrict__ scale, uint64_t seed = 0, uint64_t offset = 0)
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;
@@ -283,9 +283,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
         float s, inv;
         sym_params(a, qmax, s, inv);
         uint32_t q[E];
+        if constexpr (SR) {
+            float u[E];
+            sr_uniforms<E>(seed, offset + (uint64_t)(base + E * lane), u);
 #pragma unroll
-        for (int i = 0; i < E; ++i)
-            q[i] = code_bits(v[i], inv);
+            for (int i = 0; i < E; ++i)
+                q[i] = code_bits_sr(v[i], inv, u[i], qmax);
+        } else {
+#pragma unroll
+            for (int i = 0; i < E; ++i)
+                q[i] = code_bits(v[i], inv);
+        }
         store_codes<E, BITS>(codes + base * BITS / 8, valid, lds, q);
         const int off = E * lane;
         if (off < valid && off % group == 0)
@@ -299,10 +307,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
 // (BITS_OUT 4/8) or inverse Hadamard (block NB) + out_scale to float32
 // (BITS_OUT 0)
 // ---------------------------------------------------------------------------
-template <int BITS_IN, int BITS_OUT, int E, int NB, int PMAX, int DEPTH>
+template <int BITS_IN, int BITS_OUT, int E, int NB, int PMAX, int DEPTH, bool SR = false>
 __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
     PeerTable peers, int P, int64_t n, int group, float cn, float out_scale, uint8_t *__restrict__ out_codes,
-    float *__restrict__ out_scales, float *__restrict__ out_f32)
+    float *__restrict__ out_scales, float *__restrict__ out_f32, uint64_t seed = 0, uint64_t offset = 0)
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;
@@ -401,9 +409,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
             float s, inv;
             sym_params(a, qmax, s, inv);
             uint32_t q[E];
+            if constexpr (SR) {
+                float u[E];
+                sr_uniforms<E>(seed, offset + (uint64_t)(base + off), u);
 #pragma unroll
-            for (int i = 0; i < E; ++i)
-                q[i] = code_bits(acc[i], inv);
+                for (int i = 0; i < E; ++i)
+                    q[i] = code_bits_sr(acc[i], inv, u[i], qmax);
+            } else {
+#pragma unroll
+                for (int i = 0; i < E; ++i)
+                    q[i] = code_bits(acc[i], inv);
+            }
             store_codes<E, BITS_OUT>(out_codes + base * BITS_OUT / 8, valid, lds, q);
             if (off < valid && off % group == 0)
                 out_scales[(base + off) / group] = s;
@@ -482,19 +498,20 @@ int with_block(int nb, A... a)
 // The re-quantizing variant keeps P chunks per lane in flight already and
 // is fastest without the extra prefetch buffer (measured); the float32
 // variant prefetches.
-template <int BITS_IN, int BITS_OUT, int E, int NB>
+template <int BITS_IN, int BITS_OUT, int E, int NB, bool SR = false>
 int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, float out_scale,
-              uint8_t *out_codes, float *out_scales, float *out_f32, hipStream_t s)
+              uint8_t *out_codes, float *out_scales, float *out_f32, hipStream_t s, uint64_t seed = 0,
+              uint64_t offset = 0)
 {
     constexpr int pipe = BITS_OUT == 0 ? kDepth : 0;
     if (P <= 4)
-        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe>, wave_blocks(n, E), kCap, s, peers, P,
-                      n, group, cn, out_scale, out_codes, out_scales, out_f32);
+        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe, SR>, wave_blocks(n, E), kCap, s, peers, P,
+                      n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
     if (P <= 8)
-        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe>, wave_blocks(n, E), kCap, s, peers, P,
-                      n, group, cn, out_scale, out_codes, out_scales, out_f32);
-    return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, 0>, wave_blocks(n, E), kCap, s, peers, P, n,
-                  group, cn, out_scale, out_codes, out_scales, out_f32);
+        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe, SR>, wave_blocks(n, E), kCap, s, peers, P,
+                      n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
+    return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, 0, SR>, wave_blocks(n, E), kCap, s, peers, P, n,
+                  group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
 }
 
 } // namespace sdp4

@@ -62,6 +62,11 @@ int launch_dequant_reduce_f32_in8(const PeerTable &peers, int P, int64_t n, int 
                                   float out_scale, float *out_f32, hipStream_t s);
 int launch_dequant_reduce_f32_in4(const PeerTable &peers, int P, int64_t n, int group, int nblk, float cn,
                                   float out_scale, float *out_f32, hipStream_t s);
+int launch_grad_quant_sr(const float *x, int64_t n, int bits, int nblk, int group, float cn, uint64_t seed,
+                         uint64_t offset, uint8_t *codes, float *scale, hipStream_t s);
+int launch_dequant_reduce_sr(const PeerTable &peers, int P, int64_t n, int bits_in, int group, int bits_out,
+                             uint64_t seed, uint64_t offset, uint8_t *out_codes, float *out_scales,
+                             float *out_f32, hipStream_t s);
 int launch_hadamard(const float *x, float *y, int64_t n, int nblk, float cn, hipStream_t s);
 int launch_reduce_f32(const F32Table &xs, int P, int64_t n, float *y, hipStream_t s);
 int launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s);

@@ -90,9 +90,28 @@ class HotPath:
         sdp4.sdp4_dequant_reduce(c, s, self.m, 4, self.group, 0, block, self.out_scale, None, None,
                                  self.out, stream=stream)
 
+    # seeds of the stochastically rounded variant (first and second level)
+    SR_SEEDS = (0x5D94_0001, 0x5D94_0002)
+
+    def grad_quant_sr(self, stream=None, bits=8, block=None):
+        block = self.block if block is None else block
+        sdp4.sdp4_grad_quant_sr(self.grad, bits, block, self.group, self.SR_SEEDS[0], 0, self.c8, self.s8,
+                                stream=stream)
+
+    def reduce_intra_sr(self, stream=None, bits_in=8):
+        c, s = self.intra_chunks(bits_in)
+        sdp4.sdp4_dequant_reduce_sr(c, s, self.M, bits_in, self.group, 4, self.SR_SEEDS[1], 0, self.c4, self.s4,
+                                    stream=stream)
+
     def gradient_variant(self, name: str, stream=None):
         """The paper's gradient strategies (Sec. 5.1, Sec. 5.4) on the same kernels:
-        TLq-HS (8-bit then 4-bit, Hadamard), TLq (no Hadamard), ULq (4-bit twice, no Hadamard)."""
+        TLq-HS (8-bit then 4-bit, Hadamard), TLq (no Hadamard), ULq (4-bit twice,
+        no Hadamard), and TLq-HS with stochastic rounding at both levels."""
+        if name == "tlq_hs_sr":
+            self.grad_quant_sr(stream)
+            self.reduce_intra_sr(stream)
+            self.reduce_inter(stream)
+            return
         bits1, block = {"tlq_hs": (8, self.block), "tlq": (8, 0), "ulq": (4, 0)}[name]
         self.grad_quant(stream, bits=bits1, block=block)
         self.reduce_intra(stream, bits_in=bits1)

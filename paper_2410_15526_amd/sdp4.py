@@ -46,6 +46,9 @@ def lib() -> C.CDLL:
                 "sdp4_qwd_decode": (i32, [vp, vp, vp, i64, i32, vp, i32, vp]),
                 "sdp4_grad_quant": (i32, [vp, i64, i32, i32, i32, vp, vp, vp]),
                 "sdp4_dequant_reduce": (i32, [i32, vp, vp, i64, i32, i32, i32, i32, f32, vp, vp, vp, vp]),
+                "sdp4_grad_quant_sr": (i32, [vp, i64, i32, i32, i32, C.c_uint64, C.c_uint64, vp, vp, vp]),
+                "sdp4_dequant_reduce_sr": (i32, [i32, vp, vp, i64, i32, i32, i32, C.c_uint64, C.c_uint64, vp, vp,
+                                                 vp, vp]),
                 "sdp4_hadamard": (i32, [vp, vp, i64, i32, vp]),
                 "sdp4_reduce_f32": (i32, [i32, vp, vp, i64, vp]),
                 "sdp4_copy_f32": (i32, [vp, vp, i64, vp]),
@@ -130,6 +133,25 @@ def sdp4_dequant_reduce(codes, scales, n_chunk, bits_in, group, bits_out, hadama
         P, C.cast(cp, C.c_void_p), C.cast(sp, C.c_void_p), n_chunk, bits_in, group, bits_out,
         hadamard_block, float(out_scale), _ptr(out_codes), _ptr(out_scales), _ptr(out_f32),
         _stream(stream)))
+
+
+def sdp4_grad_quant_sr(x, bits, hadamard_block, group, seed, offset, codes, scale, n=None, stream=None):
+    """Stochastically rounded sdp4_grad_quant (unbiased; see include/sdp4.h)."""
+    n = x.numel() if n is None else n
+    _ck("sdp4_grad_quant_sr", lib().sdp4_grad_quant_sr(_ptr(x), n, bits, hadamard_block, group, seed, offset,
+                                                       _ptr(codes), _ptr(scale), _stream(stream)))
+
+
+def sdp4_dequant_reduce_sr(codes, scales, n_chunk, bits_in, group, bits_out, seed, offset, out_codes, out_scales,
+                           out_f32=None, stream=None):
+    P = len(codes)
+    if len(scales) != P:
+        raise ValueError("sdp4_dequant_reduce_sr: codes and scales differ in length")
+    cp = (C.c_void_p * max(P, 1))(*[_ptr(c) for c in codes])
+    sp = (C.c_void_p * max(P, 1))(*[_ptr(s) for s in scales])
+    _ck("sdp4_dequant_reduce_sr", lib().sdp4_dequant_reduce_sr(
+        P, C.cast(cp, C.c_void_p), C.cast(sp, C.c_void_p), n_chunk, bits_in, group, bits_out, seed, offset,
+        _ptr(out_codes), _ptr(out_scales), _ptr(out_f32), _stream(stream)))
 
 
 def sdp4_hadamard(x, y, block, n=None, stream=None):

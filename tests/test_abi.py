@@ -155,3 +155,27 @@ def test_binding_refuses_host_tensors():
     x = torch.zeros(4096)
     with pytest.raises(ValueError):
         sdp4.sdp4_grad_quant(x, 8, 256, 128, x, x)
+
+
+def test_stochastic_rounding_entry_points_validation():
+    L = sdp4.lib()
+    args = lambda **k: dict(dict(x=A, n=4096, bits=8, block=256, group=128, seed=1, offset=0, codes=B, scale=CC), **k)
+    call = lambda a: L.sdp4_grad_quant_sr(a["x"], a["n"], a["bits"], a["block"], a["group"], a["seed"], a["offset"],
+                                          a["codes"], a["scale"], None)
+    assert call(args(offset=4)) == EALIGN
+    assert call(args(offset=12)) == EALIGN
+    assert call(args(bits=2)) == EINVAL
+    assert call(args(block=96)) == EINVAL
+    assert call(args(n=0)) == OK
+    assert call(args(x=None)) == EINVAL
+    assert call(args(codes=A + 64)) == EINVAL
+    cp = (C.c_void_p * 2)(A, A + (1 << 20))
+    sp = (C.c_void_p * 2)(B, B + (1 << 20))
+    dr = lambda P=2, bits_out=4, offset=0, oc=D, os_=D + (1 << 24), n=4096: L.sdp4_dequant_reduce_sr(
+        P, C.cast(cp, C.c_void_p), C.cast(sp, C.c_void_p), n, 8, 128, bits_out, 7, offset, oc, os_, None, None)
+    assert dr(P=0) == ERANGE and dr(P=17) == ERANGE
+    assert dr(bits_out=0) == EINVAL and dr(bits_out=2) == EINVAL
+    assert dr(offset=6) == EALIGN
+    assert dr(oc=None) == EINVAL
+    assert dr(oc=A + 32) == EINVAL
+    assert dr(n=0) == OK

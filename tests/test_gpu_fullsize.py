@@ -53,29 +53,35 @@ def check_qwd(hp, w, seed, starts, L):
         assert np.array_equal(got.view(np.uint8), np.ascontiguousarray(want).view(np.uint8)), f"decode@{a}"
 
 
-def k1_ref(w, seed, a, L, bits=8, block=None):
+def k1_ref(w, seed, a, L, bits=8, block=None, sr=None):
     x = synth.gradient(w, a, L, seed)
-    return oracle.grad_quant(x, bits, w.hadamard_block if block is None else block, w.group)
+    block = w.hadamard_block if block is None else block
+    if sr is not None:                      # stochastic rounding: element offset = position a
+        return oracle.grad_quant_sr(x, bits, block, w.group, sr[0], a)
+    return oracle.grad_quant(x, bits, block, w.group)
 
 
-def k2_ref(w, seed, x, L, bits=8, block=None):
+def k2_ref(w, seed, x, L, bits=8, block=None, sr=None):
     """Oracle K2 output segment [x, x+L) of the intra-node reduction."""
     M, g = w.n // w.P, w.group
-    k1 = [k1_ref(w, seed, p * M + x, L, bits, block) for p in range(w.P)]
+    k1 = [k1_ref(w, seed, p * M + x, L, bits, block, sr) for p in range(w.P)]
+    if sr is not None:
+        return oracle.dequant_reduce_sr([c for c, _, _ in k1], [s for _, s, _ in k1], L, bits, g, 4, sr[1], x,
+                                        want_f32=False)
     return oracle.dequant_reduce([c for c, _, _ in k1], [s for _, s, _ in k1], L, bits, g, 4, want_f32=False)
 
 
-def check_gradient_path(hp, w, seed, starts_k1, starts_k3, L, bits=8, block=None):
+def check_gradient_path(hp, w, seed, starts_k1, starts_k3, L, bits=8, block=None, sr=None):
     block = w.hadamard_block if block is None else block
     g, M, m = w.group, w.n // w.P, w.n // w.P // w.Q
     for a in starts_k1:
-        rc, rs, pre = k1_ref(w, seed, a, L, bits, block)
+        rc, rs, pre = k1_ref(w, seed, a, L, bits, block, sr)
         check_codes(host(hp.c8[a * bits // 8:(a + L) * bits // 8]), rc, pre, L, bits, what=f"k1@{a}")
         check_headers(host(hp.s8[a // g:(a + L) // g]), rs, f"k1 scale@{a}")
     for a in starts_k3:
         parts = []
         for q in range(w.Q):
-            r = k2_ref(w, seed, q * m + a, L, bits, block)
+            r = k2_ref(w, seed, q * m + a, L, bits, block, sr)
             x = q * m + a
             check_codes(host(hp.c4[x // 2:(x + L) // 2]), r["codes"], r["pre"], L, 4, what=f"k2@{x}")
             check_headers(host(hp.s4[x // g:(x + L) // g]), r["scales"], f"k2 scale@{x}")
@@ -147,7 +153,7 @@ def test_full_shard_step(name):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("variant,bits,block", [("tlq", 8, 0), ("ulq", 4, 0)])
+@pytest.mark.parametrize("variant,bits,block", [("tlq", 8, 0), ("ulq", 4, 0), ("tlq_hs_sr", 8, 256)])
 def test_paper_variants_full_shard(variant, bits, block):
     """TLq (no Hadamard) and ULq (4-bit twice, no Hadamard) of Sec. 5.1 / 5.4 on
     the GPT-1.3B shard, through the same launch sequence as the benchmark."""
@@ -158,7 +164,7 @@ def test_paper_variants_full_shard(variant, bits, block):
     torch().cuda.synchronize()
     L = 4 * w.group
     check_gradient_path(hp, w, 0, segments(w.n, L, 8, 5), segments(w.n // w.P // w.Q, L, 4, 6), L,
-                        bits=bits, block=block)
+                        bits=bits, block=block, sr=HotPath.SR_SEEDS if variant.endswith("_sr") else None)
 
 
 def test_tiny_shard_step_every_element():

@@ -425,3 +425,58 @@ def test_binding_reports_status():
     with pytest.raises(sdp4.Sdp4Error) as e:
         sdp4.sdp4_grad_quant(x[:4096], 8, 256, 96, c, s)
     assert e.value.status == sdp4.EINVAL
+
+
+# ----------------------------------------------------------------------------
+# stochastic rounding (unbiased gradient compression)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("block,group", [(0, 32), (64, 128), (256, 128), (128, 512), (1024, 4096)])
+@pytest.mark.parametrize("seed,offset", [(0, 0), (0xDEADBEEF12345678, 8 * 12345), (7, 1 << 33)])
+def test_grad_quant_sr(bits, block, group, seed, offset):
+    n = size_for(max(group, block))
+    say(f"grad_quant_sr bits={bits} block={block} group={group} seed={seed} offset={offset} n={n}")
+    x = grad_input(n, seed=bits + block + group)
+    xd = dev(x)
+    codes, scale = empty(n * bits // 8, "u8"), empty(n // group, "f32")
+    sdp4.sdp4_grad_quant_sr(xd, bits, block, group, seed, offset, codes, scale)
+    sync()
+    rc, rs, pre = oracle.grad_quant_sr(x, bits, block, group, seed, offset)
+    check_headers(host(scale), rs)
+    assert np.array_equal(host(codes).view(np.uint8), rc.view(np.uint8))
+
+
+@pytest.mark.parametrize("P", [1, 3, 8, 16])
+@pytest.mark.parametrize("bits_in,bits_out", [(8, 4), (4, 4), (8, 8)])
+def test_dequant_reduce_sr(P, bits_in, bits_out):
+    group = 128
+    n = size_for(group)
+    say(f"dequant_reduce_sr P={P} in={bits_in} out={bits_out}")
+    msgs = peer_messages(P, n, bits_in, 0, group, seed=40 + P)
+    oc, os_, of = empty(n * bits_out // 8, "u8"), empty(n // group, "f32"), empty(n, "f32")
+    sdp4.sdp4_dequant_reduce_sr([dev(c) for c, _ in msgs], [dev(s) for _, s in msgs], n, bits_in, group, bits_out,
+                                99, 64, oc, os_, of)
+    sync()
+    ref = oracle.dequant_reduce_sr([c for c, _ in msgs], [s for _, s in msgs], n, bits_in, group, bits_out, 99, 64)
+    check_f32(host(of), ref["f32"])
+    check_headers(host(os_), ref["scales"])
+    assert np.array_equal(host(oc).view(np.uint8), ref["codes"].view(np.uint8))
+
+
+def test_sr_pieces_equal_one_call_and_seeds_differ():
+    n, group, block = 1 << 16, 128, 256
+    say("sr pieces")
+    x = dev(grad_input(n, seed=9))
+    whole = empty(n, "u8")
+    s = empty(n // group, "f32")
+    sdp4.sdp4_grad_quant_sr(x, 8, block, group, 5, 0, whole, s)
+    parts = empty(n, "u8")
+    h = n // 2
+    sdp4.sdp4_grad_quant_sr(x[:h], 8, block, group, 5, 0, parts[:h], s[:h // group])
+    sdp4.sdp4_grad_quant_sr(x[h:], 8, block, group, 5, h, parts[h:], s[h // group:])
+    other = empty(n, "u8")
+    sdp4.sdp4_grad_quant_sr(x, 8, block, group, 6, 0, other, s)
+    sync()
+    assert np.array_equal(host(whole), host(parts))
+    assert not np.array_equal(host(whole), host(other))
