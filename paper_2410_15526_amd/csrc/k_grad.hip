@@ -11,7 +11,7 @@ struct GradQuant {
     static int run(const float *x, int64_t n, int bits, int group, float cn, uint8_t *codes, float *scale,
                    hipStream_t s)
     {
-        if (group > 64 * 32) {
+        if (use_wide_lanes(group, SDP4_E_K1)) {
             auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth> : k_grad_quant<4, 64, NB, kDepth>;
             return launch(k, wave_blocks(n, 64), kCap, s, x, n, group, cn, codes, scale, uint64_t(0), uint64_t(0));
         }

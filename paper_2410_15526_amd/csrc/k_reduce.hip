@@ -66,7 +66,7 @@ int launch_dequant_reduce(const PeerTable &peers, int P, int64_t n, int bits_in,
         return bits_in == 8
                    ? launch_dequant_reduce_f32_in8(peers, P, n, group, nblk, cn, out_scale, out_f32, s)
                    : launch_dequant_reduce_f32_in4(peers, P, n, group, nblk, cn, out_scale, out_f32, s);
-    const bool wide = group > 64 * 32;
+    const bool wide = use_wide_lanes(group, SDP4_E_RED);
     if (bits_in == 8) {
         if (bits_out == 4)
             return wide ? dr_launch<8, 4, 64, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s)

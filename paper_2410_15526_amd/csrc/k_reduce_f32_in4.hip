@@ -11,7 +11,7 @@ struct DequantReduceF32 {
     static int run(const PeerTable &peers, int P, int64_t n, int group, float cn, float out_scale,
                    float *out_f32, hipStream_t s)
     {
-        if (group > 64 * 32)
+        if (use_wide_lanes(group, SDP4_E_RED))
             return dr_launch<4, 0, 64, NB>(peers, P, n, group, cn, out_scale, nullptr, nullptr, out_f32, s);
         return dr_launch<4, 0, 32, NB>(peers, P, n, group, cn, out_scale, nullptr, nullptr, out_f32, s);
     }

@@ -11,7 +11,7 @@ struct GradQuantSR {
     static int run(const float *x, int64_t n, int bits, int group, float cn, uint64_t seed, uint64_t offset,
                    uint8_t *codes, float *scale, hipStream_t s)
     {
-        if (group > 64 * 32) {
+        if (use_wide_lanes(group, SDP4_E_K1)) {
             auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth, true> : k_grad_quant<4, 64, NB, kDepth, true>;
             return launch(k, wave_blocks(n, 64), kCap, s, x, n, group, cn, codes, scale, seed, offset);
         }
@@ -32,7 +32,7 @@ int launch_dequant_reduce_sr(const PeerTable &peers, int P, int64_t n, int bits_
                              uint64_t seed, uint64_t offset, uint8_t *out_codes, float *out_scales,
                              float *out_f32, hipStream_t s)
 {
-    const bool wide = group > 64 * 32;
+    const bool wide = use_wide_lanes(group, SDP4_E_RED);
     if (bits_in == 8) {
         if (bits_out == 4)
             return wide ? dr_launch<8, 4, 64, 0, true>(peers, P, n, group, 1.0f, 1.0f, out_codes, out_scales, out_f32,

@@ -21,6 +21,19 @@
 #ifndef SDP4_PEER_LDS
 #define SDP4_PEER_LDS 1
 #endif
+// Elements per lane of each kernel family (32 or 64; group 4096 always uses 64).
+#ifndef SDP4_E_ENC
+#define SDP4_E_ENC 32
+#endif
+#ifndef SDP4_E_DEC
+#define SDP4_E_DEC 32
+#endif
+#ifndef SDP4_E_K1
+#define SDP4_E_K1 32
+#endif
+#ifndef SDP4_E_RED
+#define SDP4_E_RED 32
+#endif
 #ifndef SDP4_BLOCKS_PER_CU
 #define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
 #endif
@@ -471,6 +484,11 @@ inline int64_t wave_blocks(int64_t n, int E)
 }
 
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
+
+// 64 elements per lane: required for groups of 4096 (a group must fit one
+// wavefront), allowed (preferred_e == 64) for any group of at least 64 (a
+// lane slice must not straddle groups); otherwise 32.
+inline bool use_wide_lanes(int group, int preferred_e) { return group > 64 * 32 || (preferred_e == 64 && group >= 64); }
 static_assert(kBlockThreads == kLaunchThreads, "block size");
 
 // Hadamard block sizes the kernels are compiled for: 0 (none), 2 .. 1024.
