@@ -179,3 +179,19 @@ def test_stochastic_rounding_entry_points_validation():
     assert dr(oc=None) == EINVAL
     assert dr(oc=A + 32) == EINVAL
     assert dr(n=0) == OK
+
+
+def test_header_is_c99_and_a_c_program_links(tmp_path):
+    """The boundary is a C ABI: the header compiles as strict C99 and a C
+    program links against the library and gets the documented statuses."""
+    import shutil
+    if not shutil.which("gcc"):
+        pytest.skip("gcc not available")
+    exe = tmp_path / "client"
+    libdir = os.path.dirname(sdp4._LIB_PATH)
+    cmd = ["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.join(ROOT, "include"),
+           os.path.join(ROOT, "tests", "abi_c_client.c"), "-L", libdir, "-lsdp4", f"-Wl,-rpath,{libdir}",
+           "-o", str(exe)]
+    subprocess.run(cmd, check=True, capture_output=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    assert out[:10] == ["1", "2", "0", "3", "1", "2", "2048", "32", "peer count out of range", "0"]
