@@ -23,9 +23,13 @@ namespace sdp4 {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+#ifndef SDP4_WAVES_PER_BLOCK
+#define SDP4_WAVES_PER_BLOCK 4
+#endif
+
 constexpr int kWave = 64;
-constexpr int kBlockThreads = 256;
-constexpr int kWavesPerBlock = kBlockThreads / kWave;
+constexpr int kWavesPerBlock = SDP4_WAVES_PER_BLOCK; // independent wavefronts per block
+constexpr int kBlockThreads = kWave * kWavesPerBlock;
 
 SDP4_DEV int lane_id() { return __lane_id(); }
 

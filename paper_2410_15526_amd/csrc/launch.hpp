@@ -10,7 +10,10 @@
 namespace sdp4 {
 
 constexpr int kMaxPeers = 16;
-constexpr int kLaunchThreads = 256;
+#ifndef SDP4_WAVES_PER_BLOCK
+#define SDP4_WAVES_PER_BLOCK 4
+#endif
+constexpr int kLaunchThreads = 64 * SDP4_WAVES_PER_BLOCK;
 
 // Pointer tables passed by value in the kernel arguments.
 struct PeerTable {

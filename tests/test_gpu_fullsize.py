@@ -189,3 +189,19 @@ def test_tiny_shard_step_every_element():
                                [r2["scales"][q * m // g:(q + 1) * m // g] for q in range(Q)], m, 4, g, 0,
                                w.hadamard_block, 1.0 / (P * Q))
     check_f32(host(hp.out), r3["f32"])
+
+
+@pytest.mark.timeout(900)
+def test_shard_beyond_2_31_elements():
+    """64-bit indexing: one step on n = 2^31 + 2^21 elements (the GPT-1.3B
+    recipe extended to 43 layers); segments straddling and past element 2^31
+    and the last segment are checked against the oracle."""
+    w = synth.scaled(synth.WORKLOADS["c3"], (1 << 31) + (1 << 21))
+    hp = build(w, 0)
+    say(f"n = {w.n:,}: one step")
+    hp.step()
+    torch().cuda.synchronize()
+    L = 1024
+    big = [(1 << 31) - L, 1 << 31, (1 << 31) + 7 * L, w.n - L]
+    check_qwd(hp, w, 0, big, L)
+    check_gradient_path(hp, w, 0, big, segments(w.n // w.P // w.Q, L, 3, 7), L)
