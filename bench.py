@@ -117,6 +117,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
+    ap.add_argument("--no-table5", action="store_true")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -203,18 +204,19 @@ def main():
                    "unfused_gradient_ms": round(ue[2].elapsed_time(ue[3]) / 5, 4)}
 
     # the paper's ablation variants on the same kernels and the same shard
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return round(a.elapsed_time(b) / reps, 4)
+
     variants = {}
     if not args.no_variants:
-        def timed(fn, reps=5):
-            fn()
-            torch.cuda.synchronize()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            for _ in range(reps):
-                fn()
-            b.record()
-            torch.cuda.synchronize()
-            return round(a.elapsed_time(b) / reps, 4)
         for v in ("tlq_hs", "tlq", "ulq", "tlq_hs_sr"):
             variants[f"{v}_gradient_ms"] = timed(lambda: hp.gradient_variant(v))
         g2 = 2048
@@ -226,6 +228,30 @@ def main():
         zero = torch.zeros(w.n, dtype=hp.w_prev.dtype, device="cuda")
         variants["qw_g2048_encode_ms"] = timed(lambda: sdp4.sdp4_qwd_encode(hp.w_new, zero, g2, codes, sc, mn))
         del codes, sc, mn, zero
+
+    # the shape of the paper's Table 5 (one GPU, 8 MB .. 2048 MB of fp32 data): 8-bit group
+    # quantization and single-chunk dequantization to fp32, without and with a fused 32 x 32
+    # Hadamard transform (the size the paper uses), group 128; GB/s of fp32 input / output
+    table5 = {}
+    if not args.no_table5:
+        del hp
+        torch.cuda.empty_cache()
+        for mb in (8, 16, 64, 512, 1024, 2048):
+            n = mb * (1 << 20) // 4
+            x = torch.randn(n, device="cuda")
+            c = torch.empty(n, dtype=torch.uint8, device="cuda")
+            s = torch.empty(n // 128, device="cuda")
+            y = torch.empty(n, device="cuda")
+            row = {}
+            for blk in (0, 32):
+                t_q = timed(lambda: sdp4.sdp4_grad_quant(x, 8, blk, 128, c, s), reps=20)
+                t_d = timed(lambda: sdp4.sdp4_dequant_reduce([c], [s], n, 8, 128, 0, blk, 1.0, None, None, y),
+                            reps=20)
+                tag = "had" if blk else "no_had"
+                row[f"quant_{tag}_GBps"] = round(4 * n / (t_q * 1e-3) / 1e9, 1)
+                row[f"dequant_{tag}_GBps"] = round(4 * n / (t_d * 1e-3) / 1e9, 1)
+            table5[f"{mb}MB"] = row
+            del x, c, s, y
 
     traffic = traffic_for(dom)
     line = {
@@ -255,6 +281,8 @@ def main():
         line["hadamard_fusion"] = unfused
     if variants:
         line["variants"] = variants
+    if table5:
+        line["table5_sweep"] = table5
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample ...")
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_log2, args.seed)

@@ -63,7 +63,6 @@ SDP4_DEV float xor_lane(float v)
     return __builtin_bit_cast(float, r);
 }
 
-template <int E>
 SDP4_DEV void max_lanes(float &a, int lanes)
 {
     // reduce over `lanes` (power of two, 1..64) neighbouring lanes

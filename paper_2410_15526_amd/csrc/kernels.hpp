@@ -1,15 +1,19 @@
 // kernels.hpp -- gfx950 kernel templates of the SDP4Bit compression hot
 // path; the .hip files instantiate and launch them.
 //
-//
 // Every kernel is a persistent loop of wavefronts over wave tiles of 64*E
-// consecutive elements (see device.hpp for the lane layout).  Blocks have
-// four independent wavefronts, each with its own LDS staging region; no
-// kernel needs a block-wide barrier.  With PIPE set, a wave issues the
-// global loads of its next tile before it processes the current one, so
-// HBM latency overlaps the LDS transposes, the arithmetic and the stores.
+// consecutive elements (see device.hpp for the lane layout).  Blocks hold
+// independent wavefronts, each with its own LDS staging region; no kernel
+// needs a block-wide barrier.  With a prefetch depth D >= 1 a wave issues
+// the global loads of its next D tiles before it processes the current one,
+// so HBM latency overlaps the LDS transposes, the arithmetic and the stores.
 // Everything a wave computes for a tile depends on that tile alone, so
-// results do not depend on the grid size or on the pipelining.
+// results do not depend on the grid size or on the prefetching.
+//
+// The SDP4_* macros below are build-time tuning knobs; their defaults are
+// the measured best on MI355X (two resident blocks of four waves per CU,
+// one tile prefetched, 32 elements per lane, int8 peer chunks transposed
+// through LDS).
 #pragma once
 
 #include "device.hpp"
@@ -19,7 +23,7 @@
 #define SDP4_PIPE 1 // tiles prefetched ahead of the one being processed
 #endif
 #ifndef SDP4_PEER_LDS
-#define SDP4_PEER_LDS 1
+#define SDP4_PEER_LDS 1 // int8 peer chunks: coalesced loads + LDS transpose
 #endif
 // Elements per lane of each kernel family (32 or 64; group 4096 always uses 64).
 #ifndef SDP4_E_ENC
@@ -292,7 +296,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
 #pragma unroll
         for (int i = 0; i < E; ++i)
             a = fmaxf(a, fabsf(v[i]));
-        max_lanes<E>(a, lanes_per_group);
+        max_lanes(a, lanes_per_group);
         float s, inv;
         sym_params(a, qmax, s, inv);
         uint32_t q[E];
@@ -418,7 +422,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
 #pragma unroll
             for (int i = 0; i < E; ++i)
                 a = fmaxf(a, fabsf(acc[i]));
-            max_lanes<E>(a, group / E);
+            max_lanes(a, group / E);
             float s, inv;
             sym_params(a, qmax, s, inv);
             uint32_t q[E];
