@@ -60,6 +60,8 @@ def lib() -> C.CDLL:
                 "sdp4ref_unpack4": (i32, [vp, i64, i32, vp]),
                 "sdp4ref_qwd_encode": (i32, [vp, vp, i32, i64, i32, vp, vp, vp, vp]),
                 "sdp4ref_qwd_decode": (i32, [vp, vp, vp, i64, i32, vp, i32]),
+                "sdp4ref_qwd_encode_sym": (i32, [vp, vp, i32, i64, i32, vp, vp, vp]),
+                "sdp4ref_qwd_decode_sym": (i32, [vp, vp, i64, i32, vp, i32]),
                 "sdp4ref_grad_quant": (i32, [vp, i64, i32, i32, i32, vp, vp, vp]),
                 "sdp4ref_dequant_reduce": (i32, [i32, vp, vp, i64, i32, i32, i32, i32, f32,
                                                  vp, vp, vp, vp]),
@@ -214,6 +216,34 @@ def qwd_decode(codes, scale, minv, w_prev, group: int) -> np.ndarray:
     s, m = _f32(scale), _f32(minv)
     _ck(lib().sdp4ref_qwd_decode(_p(codes), _p(s), _p(m), w.size, group, _p(w), is_bf16),
         "qwd_decode")
+    return w
+
+
+def qwd_encode_sym(w_new, w_prev, group: int):
+    """Symmetric 4-bit qWD -> (codes u8[n/2] signed nibbles, scale f32[n/g], pre f32[n])."""
+    w_new = _f32(w_new)
+    w_prev = np.ascontiguousarray(w_prev)
+    is_bf16 = int(w_prev.dtype == np.uint16)
+    if not is_bf16:
+        w_prev = _f32(w_prev)
+    n = w_new.size
+    codes = np.empty(n // 2, np.uint8)
+    s = np.empty(n // group, np.float32)
+    pre = np.empty(n, np.float32)
+    _ck(lib().sdp4ref_qwd_encode_sym(_p(w_new), _p(w_prev), is_bf16, n, group, _p(codes), _p(s), _p(pre)),
+        "qwd_encode_sym")
+    return codes, s, pre
+
+
+def qwd_decode_sym(codes, scale, w_prev, group: int) -> np.ndarray:
+    """Returns the updated model weights (same dtype as ``w_prev``)."""
+    w = np.array(w_prev, copy=True)
+    is_bf16 = int(w.dtype == np.uint16)
+    if not is_bf16:
+        w = _f32(w).copy()
+    codes = np.ascontiguousarray(codes, np.uint8)
+    s = _f32(scale)
+    _ck(lib().sdp4ref_qwd_decode_sym(_p(codes), _p(s), w.size, group, _p(w), is_bf16), "qwd_decode_sym")
     return w
 
 

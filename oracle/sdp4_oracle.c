@@ -336,6 +336,62 @@ int sdp4ref_qwd_decode(const uint8_t *codes, const float *scale, const float *mi
 }
 
 /* ------------------------------------------------------------------------
+ * Symmetric qWD: the weight difference of Alg. 2 quantized with the paper's
+ * own symmetric quantizer of Sec. 2.2 at 4 bits (codes -7..7 packed as
+ * two's-complement nibbles, scale = max|d| / 7 per group, no minimum), the
+ * alternative to the asymmetric min-max codec above.
+ * codes: n/2 packed bytes; scale: n/group floats.
+ * ---------------------------------------------------------------------- */
+int sdp4ref_qwd_encode_sym(const float *w_new, const void *w_prev, int prev_is_bf16,
+                           int64_t n, int group, uint8_t *codes, float *scale, float *pre)
+{
+    if (!w_new || !w_prev || !codes || !scale || group < 2 || n % group || group % 2)
+        return REF_EINVAL;
+    float *d = malloc(sizeof(float) * (size_t)(n ? n : 1));
+    int8_t *q = malloc((size_t)(n ? n : 1));
+    if (!d || !q) {
+        free(d);
+        free(q);
+        return REF_EINVAL;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        float prev = prev_is_bf16 ? sdp4ref_bf16_to_f32(((const uint16_t *)w_prev)[i])
+                                  : ((const float *)w_prev)[i];
+        d[i] = w_new[i] - prev;
+    }
+    int rc = all_finite(d, n) ? sdp4ref_quant_sym(d, n, group, 4, q, scale, pre) : REF_ENONFINITE;
+    if (rc == REF_OK)
+        rc = sdp4ref_pack4(q, n, codes);
+    free(d);
+    free(q);
+    return rc;
+}
+
+/* Symmetric qWD decode: value = code * scale (one rounding), then the same
+ * in-place add and narrowing as sdp4ref_qwd_decode. */
+int sdp4ref_qwd_decode_sym(const uint8_t *codes, const float *scale, int64_t n, int group,
+                           void *w_prev, int prev_is_bf16)
+{
+    if (!codes || !scale || !w_prev || group < 2 || n % group || group % 2)
+        return REF_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        int c = (codes[i / 2] >> (4 * (i % 2))) & 0xF;
+        if (c >= 8)
+            c -= 16;
+        float xh = (float)c * scale[i / group];
+        if (prev_is_bf16) {
+            uint16_t *w = (uint16_t *)w_prev;
+            float sum = sdp4ref_bf16_to_f32(w[i]) + xh;
+            w[i] = sdp4ref_f32_to_bf16_rne(sum);
+        } else {
+            float *w = (float *)w_prev;
+            w[i] = w[i] + xh;
+        }
+    }
+    return REF_OK;
+}
+
+/* ------------------------------------------------------------------------
  * Gradient quantization, first level (Alg. 4: g^ <- Hadamard(grad), then
  * Quantize8Bit; with bits = 4 it is the uniform-level 4-bit variant).
  * hadamard_block = 0 skips the transform.  codes: n int8 (bits 8) or n/2

@@ -10,7 +10,7 @@ Per step:
      4 bits; "GPU" (a', b) reduces chunk a' of the 4-bit messages of every
      node (inverse Hadamard, out_scale 1/W) into its shard [b*M + a'*m, ...);
   3. main weights w <- w - eta * g;
-  4. weight communication: qWD (w~ <- w~ + C(w - w~), Alg. 3 lines 7-8), or
+  4. weight communication: qWD (w~ <- w~ + C(w - w~), the model-weight update of Alg. 3), or
      qW (w~ <- C(w), direct quantization), or none (w~ = w).
 
 Two backends compute steps 2 and 4: the CPU oracle and the HIP library.

@@ -37,9 +37,9 @@ def _naive_chain(grads, P, Q, group, block):
         deq = []
         for b in range(P):
             q8, s8, _ = oracle.quant_sym(T(grads[a][b]), group, 8)
-            deq.append(T(oracle.dequant_sym(q8, s8, group)))          # line 6 kept
+            deq.append(T(oracle.dequant_sym(q8, s8, group)))          # inverse after dequantize
         red = oracle.reduce_f32(deq)                                     # back in the plain domain
-        q4, s4, _ = oracle.quant_sym(T(red), group, 4)                   # line 8 kept
+        q4, s4, _ = oracle.quant_sym(T(red), group, 4)                   # forward before re-quantize
         level2.append((q4, s4))
     m = M // Q
     parts = [T(oracle.dequant_sym(q4[:m], s4[:m // group], group)) for (q4, s4) in level2]
