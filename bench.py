@@ -228,6 +228,8 @@ def main():
         zero = torch.zeros(w.n, dtype=hp.w_prev.dtype, device="cuda")
         variants["qw_g2048_encode_ms"] = timed(lambda: sdp4.sdp4_qwd_encode(hp.w_new, zero, g2, codes, sc, mn))
         del codes, sc, mn, zero
+        variants["qwd_sym_encode_ms"] = timed(hp.qwd_encode_sym)
+        variants["qwd_sym_decode_ms"] = timed(hp.qwd_decode_sym)
 
     # the shape of the paper's Table 5 (one GPU, 8 MB .. 2048 MB of fp32 data): 8-bit group
     # quantization and single-chunk dequantization to fp32, without and with a fused 32 x 32

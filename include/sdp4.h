@@ -131,6 +131,35 @@ int sdp4_qwd_decode(const uint8_t *codes, const float *scale, const float *minv,
                     int group, void *w_prev, int prev_dtype, void *stream);
 
 /*
+ * Symmetric qWD encode -- the weight difference of Alg. 2 quantized with the
+ * paper's own symmetric quantizer of Sec. 2.2 at 4 bits instead of the
+ * asymmetric min-max codec:
+ *      s = max |d| per group, scale = s / 7, inv = 7 / s,
+ *      code = clamp(rint(d * inv), -7, 7), value = code * scale;
+ *      a group with s = 0 has scale 0 and all-zero codes.
+ *
+ *   w_new, w_prev, prev_dtype, n, group   as for sdp4_qwd_encode
+ *   codes   [n/2] uint8        out: packed two's-complement nibbles
+ *                              (even element in the low nibble; -8 unused)
+ *   scale   [n/group] float32  out: s / 7 of each group
+ * The message is 4 + 32/group bits per element (no minimum).  Inputs are
+ * not modified.  Errors: EINVAL, EALIGN, EHIP as for sdp4_qwd_encode.
+ */
+int sdp4_qwd_encode_sym(const float *w_new, const void *w_prev, int prev_dtype, int64_t n, int group,
+                        uint8_t *codes, float *scale, void *stream);
+
+/*
+ * Symmetric qWD decode: w_prev[i] <- narrow(widen(w_prev[i]) + code[i] *
+ * scale[i / group]) in place (the product and the sum each round once).
+ *
+ *   codes, scale   a message produced by sdp4_qwd_encode_sym
+ *   n, group, w_prev, prev_dtype   as for sdp4_qwd_decode
+ * Errors: EINVAL, EALIGN, EHIP.  w_prev must not overlap the message.
+ */
+int sdp4_qwd_decode_sym(const uint8_t *codes, const float *scale, int64_t n, int group, void *w_prev,
+                        int prev_dtype, void *stream);
+
+/*
  * Gradient quantization, first level -- Alg. 4, g^ <- Hadamard(grad) then
  * Quantize8Bit (bits = 8, TLq-HS); bits = 4 gives the uniform-level 4-bit
  * variant (ULq), hadamard_block = 0 the variant without smoother (TLq).

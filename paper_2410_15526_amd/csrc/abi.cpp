@@ -92,6 +92,61 @@ int check_reduce_args(int P, const void *const *codes, const float *const *scale
     return SDP4_OK;
 }
 
+// qWD encode / decode with either codec; minv is used (and checked) only by
+// the asymmetric one, the symmetric entry points pass null.
+int qwd_encode(const float *w_new, const void *w_prev, int prev_dtype, int64_t n, int group,
+               uint8_t *codes, float *scale, float *minv, bool sym, void *stream)
+{
+    if (n < 0 || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
+        return SDP4_EINVAL;
+    if (n % group)
+        return SDP4_EALIGN;
+    if (n == 0)
+        return SDP4_OK;
+    if (!w_new || !w_prev || !codes || !scale || (!sym && !minv))
+        return SDP4_EINVAL;
+    if (!aligned(w_new, 16) || !aligned(w_prev, 16) || !aligned(codes, 16) || !aligned(scale, 4) ||
+        (minv && !aligned(minv, 4)))
+        return SDP4_EALIGN;
+    const int64_t esz = prev_dtype == SDP4_BF16 ? 2 : 4;
+    const int64_t ng = n / group;
+    const void *outs[3] = {codes, scale, minv};
+    const int64_t outn[3] = {n / 2, 4 * ng, 4 * ng};
+    for (int i = 0; i < 3; ++i) {
+        if (!outs[i])
+            continue;
+        if (overlap(outs[i], outn[i], w_new, 4 * n) || overlap(outs[i], outn[i], w_prev, esz * n))
+            return SDP4_EINVAL;
+        for (int j = 0; j < i; ++j)
+            if (overlap(outs[i], outn[i], outs[j], outn[j]))
+                return SDP4_EINVAL;
+    }
+    return sdp4::launch_qwd_encode(w_new, w_prev, prev_dtype == SDP4_BF16, sym, n, group, codes, scale,
+                                   minv, as_stream(stream));
+}
+
+int qwd_decode(const uint8_t *codes, const float *scale, const float *minv, int64_t n, int group,
+               void *w_prev, int prev_dtype, bool sym, void *stream)
+{
+    if (n < 0 || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
+        return SDP4_EINVAL;
+    if (n % group)
+        return SDP4_EALIGN;
+    if (n == 0)
+        return SDP4_OK;
+    if (!codes || !scale || !w_prev || (!sym && !minv))
+        return SDP4_EINVAL;
+    if (!aligned(codes, 16) || !aligned(w_prev, 16) || !aligned(scale, 4) || (minv && !aligned(minv, 4)))
+        return SDP4_EALIGN;
+    const int64_t esz = prev_dtype == SDP4_BF16 ? 2 : 4;
+    const int64_t ng = n / group;
+    if (overlap(w_prev, esz * n, codes, n / 2) || overlap(w_prev, esz * n, scale, 4 * ng) ||
+        (minv && overlap(w_prev, esz * n, minv, 4 * ng)))
+        return SDP4_EINVAL;
+    return sdp4::launch_qwd_decode(codes, scale, minv, n, group, w_prev, prev_dtype == SDP4_BF16, sym,
+                                   as_stream(stream));
+}
+
 } // namespace
 
 extern "C" {
@@ -99,52 +154,25 @@ extern "C" {
 int sdp4_qwd_encode(const float *w_new, const void *w_prev, int prev_dtype, int64_t n, int group,
                     uint8_t *codes, float *scale, float *minv, void *stream)
 {
-    if (n < 0 || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
-        return SDP4_EINVAL;
-    if (n % group)
-        return SDP4_EALIGN;
-    if (n == 0)
-        return SDP4_OK;
-    if (!w_new || !w_prev || !codes || !scale || !minv)
-        return SDP4_EINVAL;
-    if (!aligned(w_new, 16) || !aligned(w_prev, 16) || !aligned(codes, 16) || !aligned(scale, 4) ||
-        !aligned(minv, 4))
-        return SDP4_EALIGN;
-    const int64_t esz = prev_dtype == SDP4_BF16 ? 2 : 4;
-    const int64_t ng = n / group;
-    const void *outs[3] = {codes, scale, minv};
-    const int64_t outn[3] = {n / 2, 4 * ng, 4 * ng};
-    for (int i = 0; i < 3; ++i) {
-        if (overlap(outs[i], outn[i], w_new, 4 * n) || overlap(outs[i], outn[i], w_prev, esz * n))
-            return SDP4_EINVAL;
-        for (int j = 0; j < i; ++j)
-            if (overlap(outs[i], outn[i], outs[j], outn[j]))
-                return SDP4_EINVAL;
-    }
-    return sdp4::launch_qwd_encode(w_new, w_prev, prev_dtype == SDP4_BF16, n, group, codes, scale,
-                                   minv, as_stream(stream));
+    return qwd_encode(w_new, w_prev, prev_dtype, n, group, codes, scale, minv, false, stream);
 }
 
 int sdp4_qwd_decode(const uint8_t *codes, const float *scale, const float *minv, int64_t n,
                     int group, void *w_prev, int prev_dtype, void *stream)
 {
-    if (n < 0 || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
-        return SDP4_EINVAL;
-    if (n % group)
-        return SDP4_EALIGN;
-    if (n == 0)
-        return SDP4_OK;
-    if (!codes || !scale || !minv || !w_prev)
-        return SDP4_EINVAL;
-    if (!aligned(codes, 16) || !aligned(w_prev, 16) || !aligned(scale, 4) || !aligned(minv, 4))
-        return SDP4_EALIGN;
-    const int64_t esz = prev_dtype == SDP4_BF16 ? 2 : 4;
-    const int64_t ng = n / group;
-    if (overlap(w_prev, esz * n, codes, n / 2) || overlap(w_prev, esz * n, scale, 4 * ng) ||
-        overlap(w_prev, esz * n, minv, 4 * ng))
-        return SDP4_EINVAL;
-    return sdp4::launch_qwd_decode(codes, scale, minv, n, group, w_prev, prev_dtype == SDP4_BF16,
-                                   as_stream(stream));
+    return qwd_decode(codes, scale, minv, n, group, w_prev, prev_dtype, false, stream);
+}
+
+int sdp4_qwd_encode_sym(const float *w_new, const void *w_prev, int prev_dtype, int64_t n, int group,
+                        uint8_t *codes, float *scale, void *stream)
+{
+    return qwd_encode(w_new, w_prev, prev_dtype, n, group, codes, scale, nullptr, true, stream);
+}
+
+int sdp4_qwd_decode_sym(const uint8_t *codes, const float *scale, int64_t n, int group, void *w_prev,
+                        int prev_dtype, void *stream)
+{
+    return qwd_decode(codes, scale, nullptr, n, group, w_prev, prev_dtype, true, stream);
 }
 
 int sdp4_grad_quant(const float *x, int64_t n, int bits, int hadamard_block, int group, void *codes,

@@ -113,9 +113,11 @@ SDP4_DEV void maybe_fwht(float (&v)[E], float cn)
 }
 
 // ---------------------------------------------------------------------------
-// qWD encode: d = w_new - widen(w_prev); asymmetric 4-bit codes per group
+// qWD encode: d = w_new - widen(w_prev); 4-bit codes per group, asymmetric
+// (codes 0..15, scale and minimum) or, with SYM, symmetric (codes -7..7,
+// scale only; minv is not touched)
 // ---------------------------------------------------------------------------
-template <bool BF16, int E, int DEPTH>
+template <bool BF16, bool SYM, int E, int DEPTH>
 __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
     const float *__restrict__ w_new, const void *__restrict__ w_prev, int64_t n, int group,
     uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv)
@@ -162,6 +164,24 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
 #pragma unroll
         for (int i = 0; i < E; ++i)
             d[i] = d[i] - p[i];
+        const int off = E * lane;
+        if constexpr (SYM) {
+            float a = 0.0f;
+#pragma unroll
+            for (int i = 0; i < E; ++i)
+                a = fmaxf(a, fabsf(d[i]));
+            max_lanes(a, lanes_per_group);
+            float s, inv;
+            sym_params(a, 7.0f, s, inv);
+            uint32_t q[E];
+#pragma unroll
+            for (int i = 0; i < E; ++i)
+                q[i] = code_bits(d[i], inv);
+            store_codes<E, 4>(codes + base / 2, valid, lds, q);
+            if (off < valid && off % group == 0)
+                scale[(base + off) / group] = s;
+            return;
+        }
         float mn = d[0], mx = d[0];
 #pragma unroll
         for (int i = 1; i < E; ++i) {
@@ -179,7 +199,6 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
         for (int i = 0; i < E; ++i)
             q[i] = code_bits(d[i] - mn, inv);
         store_codes<E, 4>(codes + base / 2, valid, lds, q);
-        const int off = E * lane;
         if (off < valid && off % group == 0) {
             const int64_t gi = (base + off) / group;
             scale[gi] = s;
@@ -190,9 +209,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
 }
 
 // ---------------------------------------------------------------------------
-// qWD decode: w_prev <- narrow(widen(w_prev) + fma(code, scale, min))
+// qWD decode: w_prev <- narrow(widen(w_prev) + value) with value =
+// fma(code, scale, min), or with SYM value = code * scale (signed codes,
+// minv not read)
 // ---------------------------------------------------------------------------
-template <bool BF16, int E, int DEPTH>
+template <bool BF16, bool SYM, int E, int DEPTH>
 __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const float *__restrict__ minv, int64_t n, int group, void *__restrict__ w_prev)
@@ -218,7 +239,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
                 in.c[k] = __builtin_nontemporal_load(src + k);
             const int64_t gi = (base + off) / group;
             in.s = scale[gi];
-            in.mn = minv[gi];
+            in.mn = SYM ? 0.0f : minv[gi];
         } else {
 #pragma unroll
             for (int k = 0; k < E / 32; ++k)
@@ -246,8 +267,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
 #pragma unroll
         for (int i = 0; i < E; ++i) {
             const uint32_t word = in.c[i / 32][(i / 8) % 4];
-            const float code = (float)((word >> (4 * (i % 8))) & 0xFu);
-            w[i] = w[i] + __builtin_fmaf(code, in.s, in.mn);
+            if constexpr (SYM) {
+                const float code = (float)((int32_t)(word << (28 - 4 * (i % 8))) >> 28);
+                const float value = code * in.s;
+                w[i] = w[i] + value;
+            } else {
+                const float code = (float)((word >> (4 * (i % 8))) & 0xFu);
+                w[i] = w[i] + __builtin_fmaf(code, in.s, in.mn);
+            }
         }
         if constexpr (BF16) {
             f32_to_bf16_chunks<E>(w, c);

@@ -52,10 +52,10 @@ int launch(void (*kernel)(Params...), int64_t nwork_blocks, int per_cu_cap, hipS
     return 0;
 }
 
-int launch_qwd_encode(const float *w_new, const void *w_prev, bool bf16, int64_t n, int group,
+int launch_qwd_encode(const float *w_new, const void *w_prev, bool bf16, bool sym, int64_t n, int group,
                       uint8_t *codes, float *scale, float *minv, hipStream_t s);
 int launch_qwd_decode(const uint8_t *codes, const float *scale, const float *minv, int64_t n,
-                      int group, void *w_prev, bool bf16, hipStream_t s);
+                      int group, void *w_prev, bool bf16, bool sym, hipStream_t s);
 int launch_grad_quant(const float *x, int64_t n, int bits, int nblk, int group, float cn,
                       uint8_t *codes, float *scale, hipStream_t s);
 int launch_dequant_reduce(const PeerTable &peers, int P, int64_t n, int bits_in, int group,

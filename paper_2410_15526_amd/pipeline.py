@@ -64,6 +64,13 @@ class HotPath:
     def qwd_decode(self, stream=None):
         sdp4.sdp4_qwd_decode(self.qcodes, self.qscale, self.qmin, self.qwd_group, self.w_prev, stream=stream)
 
+    def qwd_encode_sym(self, stream=None):
+        """The symmetric 4-bit codec (scale only) in place of the min-max one."""
+        sdp4.sdp4_qwd_encode_sym(self.w_new, self.w_prev, self.qwd_group, self.qcodes, self.qscale, stream=stream)
+
+    def qwd_decode_sym(self, stream=None):
+        sdp4.sdp4_qwd_decode_sym(self.qcodes, self.qscale, self.qwd_group, self.w_prev, stream=stream)
+
     def grad_quant(self, stream=None, bits=8, block=None):
         block = self.block if block is None else block
         sdp4.sdp4_grad_quant(self.grad, bits, block, self.group, self.c8, self.s8, stream=stream)

@@ -44,6 +44,8 @@ def lib() -> C.CDLL:
             sig = {
                 "sdp4_qwd_encode": (i32, [vp, vp, i32, i64, i32, vp, vp, vp, vp]),
                 "sdp4_qwd_decode": (i32, [vp, vp, vp, i64, i32, vp, i32, vp]),
+                "sdp4_qwd_encode_sym": (i32, [vp, vp, i32, i64, i32, vp, vp, vp]),
+                "sdp4_qwd_decode_sym": (i32, [vp, vp, i64, i32, vp, i32, vp]),
                 "sdp4_grad_quant": (i32, [vp, i64, i32, i32, i32, vp, vp, vp]),
                 "sdp4_dequant_reduce": (i32, [i32, vp, vp, i64, i32, i32, i32, i32, f32, vp, vp, vp, vp]),
                 "sdp4_grad_quant_sr": (i32, [vp, i64, i32, i32, i32, C.c_uint64, C.c_uint64, vp, vp, vp]),
@@ -113,6 +115,20 @@ def sdp4_qwd_decode(codes, scale, minv, group, w_prev, n=None, stream=None):
     n = w_prev.numel() if n is None else n
     _ck("sdp4_qwd_decode", lib().sdp4_qwd_decode(_ptr(codes), _ptr(scale), _ptr(minv), n, group,
                                                  _ptr(w_prev), _prev_dtype(w_prev), _stream(stream)))
+
+
+def sdp4_qwd_encode_sym(w_new, w_prev, group, codes, scale, n=None, stream=None):
+    """codes/scale <- symmetric 4-bit quantized (w_new - w_prev); see include/sdp4.h."""
+    n = w_new.numel() if n is None else n
+    _ck("sdp4_qwd_encode_sym", lib().sdp4_qwd_encode_sym(_ptr(w_new), _ptr(w_prev), _prev_dtype(w_prev), n, group,
+                                                         _ptr(codes), _ptr(scale), _stream(stream)))
+
+
+def sdp4_qwd_decode_sym(codes, scale, group, w_prev, n=None, stream=None):
+    """w_prev <- w_prev + dequantized symmetric message, in place."""
+    n = w_prev.numel() if n is None else n
+    _ck("sdp4_qwd_decode_sym", lib().sdp4_qwd_decode_sym(_ptr(codes), _ptr(scale), n, group, _ptr(w_prev),
+                                                         _prev_dtype(w_prev), _stream(stream)))
 
 
 def sdp4_grad_quant(x, bits, hadamard_block, group, codes, scale, n=None, stream=None):

@@ -97,6 +97,35 @@ def test_qwd_decode_validation(kw, want):
     assert dec(**kw) == want
 
 
+def enc_sym(w_new=A, w_prev=B, dt=0, n=4096, group=128, codes=CC, scale=D):
+    return sdp4.lib().sdp4_qwd_encode_sym(w_new, w_prev, dt, n, group, codes, scale, None)
+
+
+def dec_sym(codes=A, scale=B, n=4096, group=128, w=CC, dt=0):
+    return sdp4.lib().sdp4_qwd_decode_sym(codes, scale, n, group, w, dt, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dt=2), EINVAL), (dict(group=100), EINVAL), (dict(group=8192), EINVAL), (dict(n=4000), EALIGN),
+    (dict(n=-128), EINVAL), (dict(w_new=None), EINVAL), (dict(w_prev=None), EINVAL), (dict(codes=None), EINVAL),
+    (dict(scale=None), EINVAL), (dict(w_prev=B + 2), EALIGN), (dict(codes=CC + 4), EALIGN),
+    (dict(scale=D + 1), EALIGN), (dict(codes=A + 16), EINVAL), (dict(scale=CC + 100 * 16), EINVAL),
+    (dict(scale=B + 4 * 100, dt=1), EINVAL), (dict(n=0), OK), (dict(n=0, w_new=None, codes=None), OK),
+])
+def test_qwd_encode_sym_validation(kw, want):
+    assert enc_sym(**kw) == want
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dt=7), EINVAL), (dict(group=96), EINVAL), (dict(n=4096 + 64), EALIGN), (dict(w=None), EINVAL),
+    (dict(codes=None), EINVAL), (dict(scale=None), EINVAL), (dict(w=CC + 8), EALIGN),
+    (dict(codes=A + 8), EALIGN), (dict(scale=B + 2), EALIGN), (dict(w=A + 512), EINVAL),
+    (dict(scale=CC + 100), EINVAL), (dict(n=0), OK),
+])
+def test_qwd_decode_sym_validation(kw, want):
+    assert dec_sym(**kw) == want
+
+
 def dr(P=4, codes=None, scales=None, n=4096, bits_in=8, group=128, bits_out=4, block=0, out_scale=1.0,
        oc=D, os_=D + (1 << 24), of=None, table_null=False):
     if codes is None:

@@ -135,6 +135,20 @@ def test_full_shard_step(name):
                 check_codes(host(codes[a // 2:(a + Lq) // 2]), rc, pre, Lq, 4, signed=False)
                 check_headers(host(sc[a // qg:(a + Lq) // qg]), rs)
                 check_headers(host(mn[a // qg:(a + Lq) // qg]), rm)
+        say("c4 symmetric qWD group 128")
+        g = 128
+        fill(hp.w_prev, lambda s, k: synth.prev_weights(w, s, k, seed), w.n)
+        hp.qwd_encode_sym()
+        hp.qwd_decode_sym()
+        torch().cuda.synchronize()
+        for a in segments(w.n, 4 * g, 8, 12):
+            Lq = 4 * g
+            prev = synth.prev_weights(w, a, Lq, seed)
+            rc, rs, pre = oracle.qwd_encode_sym(synth.new_weights(w, a, Lq, seed), prev, g)
+            check_codes(host(hp.qcodes[a // 2:(a + Lq) // 2]), rc, pre, Lq, 4, what=f"qwd sym@{a}")
+            check_headers(host(hp.qscale[a // g:(a + Lq) // g]), rs)
+            want = oracle.qwd_decode_sym(rc, rs, prev, g)
+            assert np.array_equal(host(hp.w_prev[a:a + Lq]), want), f"qwd sym decode@{a}"
     if name == "c5":
         # the float32 model-weight variant of qWD at the full size
         say("c5 qWD with float32 model weights")

@@ -103,8 +103,8 @@ def test_dequant_reduce_random(P, bits_in, bits_out, log_group, log_block, segme
 
 @SETTINGS
 @given(bf16=st.booleans(), log_group=st.integers(5, 12), segments=st.integers(1, 40),
-       kind=st.sampled_from(DISTS), seed=st.integers(0, 2 ** 31 - 1))
-def test_qwd_random(bf16, log_group, segments, kind, seed):
+       kind=st.sampled_from(DISTS), seed=st.integers(0, 2 ** 31 - 1), sym=st.booleans())
+def test_qwd_random(bf16, log_group, segments, kind, seed, sym):
     group = 1 << log_group
     n = group * segments
     r = np.random.default_rng(seed)
@@ -117,6 +117,17 @@ def test_qwd_random(bf16, log_group, segments, kind, seed):
         widened = base
     new = (widened + draw_values(kind, n, seed + 1) * np.float32(1e-3)).astype(np.float32)
     pd = dev(prev)
+    if sym:
+        codes, scale = empty(n // 2, "u8"), empty(n // group, "f32")
+        sdp4.sdp4_qwd_encode_sym(dev(new), pd, group, codes, scale)
+        sdp4.sdp4_qwd_decode_sym(codes, scale, group, pd)
+        sync()
+        rc, rs, pre = oracle.qwd_encode_sym(new, prev, group)
+        check_headers(host(scale), rs)
+        check_codes(host(codes), rc, pre, n, 4)
+        want = oracle.qwd_decode_sym(rc, rs, prev, group)
+        assert np.array_equal(host(pd).view(np.uint8), np.ascontiguousarray(want).view(np.uint8))
+        return
     codes, scale, minv = empty(n // 2, "u8"), empty(n // group, "f32"), empty(n // group, "f32")
     sdp4.sdp4_qwd_encode(dev(new), pd, group, codes, scale, minv)
     sdp4.sdp4_qwd_decode(codes, scale, minv, group, pd)

@@ -184,6 +184,66 @@ def test_qw_variant_is_encode_from_zero():
     check_f32(upd, oracle.qwd_decode(rc, rs, rm, zero, g))
 
 
+def run_qwd_sym(new, prev, group):
+    n = new.size
+    nd, pd = dev(new), dev(prev)
+    codes, scale = empty(n // 2, "u8"), empty(n // group, "f32")
+    sdp4.sdp4_qwd_encode_sym(nd, pd, group, codes, scale)
+    sdp4.sdp4_qwd_decode_sym(codes, scale, group, pd)
+    sync()
+    return host(codes), host(scale), host(pd)
+
+
+def check_qwd_sym(new, prev, group, codes, scale, upd):
+    rc, rs, pre = oracle.qwd_encode_sym(new, prev, group)
+    check_headers(scale, rs)
+    check_codes(codes, rc, pre, new.size, 4)
+    want = oracle.qwd_decode_sym(rc, rs, prev, group)
+    if prev.dtype == np.uint16:
+        assert np.array_equal(upd, want)
+    else:
+        check_f32(upd, want, "updated weights")
+
+
+@pytest.mark.parametrize("prev_dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("group", [32, 64, 128, 256, 1024, 2048, 4096])
+def test_qwd_sym_encode_decode(prev_dtype, group):
+    """Symmetric 4-bit qWD (the Sec. 2.2 quantizer on the weight difference)."""
+    n = size_for(group)
+    say(f"qwd sym prev={prev_dtype} group={group} n={n}")
+    new, prev = qwd_inputs(n, prev_dtype, seed=group + 1)
+    check_qwd_sym(new, prev, group, *run_qwd_sym(new, prev, group))
+
+
+def test_qwd_sym_decode_stage_isolated():
+    """Decode of the oracle's own symmetric message: bit-exact for both dtypes."""
+    n, group = size_for(128), 128
+    for prev_dtype in ("f32", "bf16"):
+        say(f"qwd sym decode isolated prev={prev_dtype}")
+        new, prev = qwd_inputs(n, prev_dtype, seed=5)
+        rc, rs, _ = oracle.qwd_encode_sym(new, prev, group)
+        pd = dev(prev)
+        sdp4.sdp4_qwd_decode_sym(dev(rc), dev(rs), group, pd)
+        sync()
+        want = oracle.qwd_decode_sym(rc, rs, prev, group)
+        assert np.array_equal(host(pd).view(np.uint8), np.ascontiguousarray(want).view(np.uint8))
+
+
+@pytest.mark.parametrize("prev_dtype", ["f32", "bf16"])
+def test_qwd_sym_edge_values(prev_dtype):
+    n, g = size_for(128, 4096), 128
+    say(f"qwd sym edge prev={prev_dtype}")
+    new, prev = qwd_inputs(n, prev_dtype, seed=10)
+    base = synth.bf16_bits_to_f32(prev) if prev_dtype == "bf16" else prev
+    new = new.copy()
+    new[0:g] = base[0:g]                                  # zero difference
+    new[g:2 * g] = base[g:2 * g] + np.float32(1e-3)       # (nearly) constant difference
+    new[2 * g:3 * g] = base[2 * g:3 * g] + np.float32(1e30) * np.sign(np.arange(g) - 60)
+    new[3 * g:4 * g] = base[3 * g:4 * g] + np.float32(1e-42)
+    new[4 * g] = base[4 * g] - np.float32(5.0)            # one large negative update in a group
+    check_qwd_sym(new, prev, g, *run_qwd_sym(new, prev, g))
+
+
 # ----------------------------------------------------------------------------
 # K2 / K3: dequantize + reduce
 # ----------------------------------------------------------------------------
