@@ -257,6 +257,10 @@ SDP4_DEV void fwht_lane(float (&v)[E], float cn)
         v[i] = v[i] * cn;
 }
 
+// log2 of a group size (a power of two, checked on the host): header indices
+// are shifts instead of runtime 64-bit divisions.
+SDP4_DEV int group_shift(int group) { return __builtin_ctz((unsigned)group); }
+
 // ---------------------------------------------------------------------------
 // quantize and pack
 // ---------------------------------------------------------------------------

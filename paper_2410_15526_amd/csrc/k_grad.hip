@@ -11,12 +11,16 @@ struct GradQuant {
     static int run(const float *x, int64_t n, int bits, int group, float cn, uint8_t *codes, float *scale,
                    hipStream_t s)
     {
-        if (use_wide_lanes(group, SDP4_E_K1)) {
-            auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth> : k_grad_quant<4, 64, NB, kDepth>;
-            return launch(k, wave_blocks(n, 64), kCap, s, x, n, group, cn, codes, scale, uint64_t(0), uint64_t(0));
+        if (use_wide_lanes(group, SDP4_E_K1)) {   // 64 elements per lane: the default shape's register budget
+            constexpr int WPB = kWavesPerBlock;
+            auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth, WPB> : k_grad_quant<4, 64, NB, kDepth, WPB>;
+            return launch<WPB>(k, wave_blocks<WPB>(n, 64), kCap, s, x, n, group, cn, codes, scale, uint64_t(0),
+                               uint64_t(0));
         }
-        auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth> : k_grad_quant<4, 32, NB, kDepth>;
-        return launch(k, wave_blocks(n, 32), kCap, s, x, n, group, cn, codes, scale, uint64_t(0), uint64_t(0));
+        constexpr int WPB = kK1Waves;
+        auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth, WPB> : k_grad_quant<4, 32, NB, kDepth, WPB>;
+        return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, uint64_t(0),
+                           uint64_t(0));
     }
 };
 
@@ -27,7 +31,8 @@ struct Hadamard {
         if constexpr (NB < 2)
             return 1;
         else
-            return launch(k_hadamard<32, NB, kDepth>, wave_blocks(n, 32), kCap, s, x, y, n, cn);
+            return launch<kWavesPerBlock>(k_hadamard<32, NB, kDepth, kWavesPerBlock>, wave_blocks<kWavesPerBlock>(n, 32),
+                                          kCap, s, x, y, n, cn);
     }
 };
 

@@ -10,18 +10,20 @@ template <int E>
 int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, int64_t n, int group,
                  uint8_t *codes, float *scale, float *minv, hipStream_t s)
 {
-    auto k = bf16 ? (sym ? k_qwd_encode<true, true, E, kDepth> : k_qwd_encode<true, false, E, kDepth>)
-                  : (sym ? k_qwd_encode<false, true, E, kDepth> : k_qwd_encode<false, false, E, kDepth>);
-    return launch(k, wave_blocks(n, E), kCap, s, w_new, w_prev, n, group, codes, scale, minv);
+    constexpr int WPB = kEncWaves;
+    auto k = bf16 ? (sym ? k_qwd_encode<true, true, E, kDepth, WPB> : k_qwd_encode<true, false, E, kDepth, WPB>)
+                  : (sym ? k_qwd_encode<false, true, E, kDepth, WPB> : k_qwd_encode<false, false, E, kDepth, WPB>);
+    return launch<WPB>(k, wave_blocks<WPB>(n, E), kEncCap, s, w_new, w_prev, n, group, codes, scale, minv);
 }
 
 template <int E>
 int qwd_decode_e(const uint8_t *codes, const float *scale, const float *minv, int64_t n, int group,
                  void *w_prev, bool bf16, bool sym, hipStream_t s)
 {
-    auto k = bf16 ? (sym ? k_qwd_decode<true, true, E, kDepth> : k_qwd_decode<true, false, E, kDepth>)
-                  : (sym ? k_qwd_decode<false, true, E, kDepth> : k_qwd_decode<false, false, E, kDepth>);
-    return launch(k, wave_blocks(n, E), kCap, s, codes, scale, minv, n, group, w_prev);
+    constexpr int WPB = kWavesPerBlock;
+    auto k = bf16 ? (sym ? k_qwd_decode<true, true, E, kDepth, WPB> : k_qwd_decode<true, false, E, kDepth, WPB>)
+                  : (sym ? k_qwd_decode<false, true, E, kDepth, WPB> : k_qwd_decode<false, false, E, kDepth, WPB>);
+    return launch<WPB>(k, wave_blocks<WPB>(n, E), kCap, s, codes, scale, minv, n, group, w_prev);
 }
 
 } // namespace

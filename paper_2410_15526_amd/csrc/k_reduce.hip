@@ -84,13 +84,13 @@ int launch_dequant_reduce(const PeerTable &peers, int P, int64_t n, int bits_in,
 int launch_reduce_f32(const F32Table &xs, int P, int64_t n, float *y, hipStream_t s)
 {
     const int64_t blocks = (n / 4 + kBlockThreads - 1) / kBlockThreads;
-    return launch(k_reduce_f32, blocks > 0 ? blocks : 1, 0, s, xs, P, n, y);
+    return launch<kWavesPerBlock>(k_reduce_f32, blocks > 0 ? blocks : 1, 0, s, xs, P, n, y);
 }
 
 int launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s)
 {
     const int64_t chunks = n / 4 / (kBlockThreads * 4);
-    return launch(k_copy_f32, chunks > 0 ? chunks : 1, 2, s, x, y, n);
+    return launch<kWavesPerBlock>(k_copy_f32, chunks > 0 ? chunks : 1, 2, s, x, y, n);
 }
 
 } // namespace sdp4

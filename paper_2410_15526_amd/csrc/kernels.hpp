@@ -11,9 +11,12 @@
 // results do not depend on the grid size or on the prefetching.
 //
 // The SDP4_* macros below are build-time tuning knobs; their defaults are
-// the measured best on MI355X (two resident blocks of four waves per CU,
-// one tile prefetched, 32 elements per lane, int8 peer chunks transposed
-// through LDS).
+// the measured best on MI355X: one tile prefetched, 32 elements per lane,
+// int8 peer chunks transposed through LDS, and per kernel family a block
+// shape -- one resident block of four waves per CU for the qWD encoder, one
+// block of eight waves for K1, two blocks of four waves for the rest.  (How
+// many bytes a CU keeps in flight, and how far compute spreads its requests
+// out, moves the mixed read/write bandwidth of HBM by several per cent.)
 #pragma once
 
 #include "device.hpp"
@@ -41,22 +44,37 @@
 #ifndef SDP4_BLOCKS_PER_CU
 #define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
 #endif
+// Block shape (waves per block, resident blocks per compute unit) of the qWD
+// encoder and of K1; every other kernel uses SDP4_WAVES_PER_BLOCK (device.hpp)
+// and SDP4_BLOCKS_PER_CU.
+#ifndef SDP4_ENC_WAVES
+#define SDP4_ENC_WAVES 4
+#endif
+#ifndef SDP4_ENC_BPC
+#define SDP4_ENC_BPC 1
+#endif
+#ifndef SDP4_K1_WAVES
+#define SDP4_K1_WAVES 8
+#endif
+#ifndef SDP4_K1_BPC
+#define SDP4_K1_BPC 1
+#endif
 
 namespace sdp4 {
 
 constexpr int kDepth = SDP4_PIPE;
 
 // Persistent loop of one wavefront over its tiles t, t + S, t + 2S, ...
-// (S = waves in the grid).  DEPTH = 0 loads and processes one tile at a
+// (S = waves in the grid, WPB waves per block).  DEPTH = 0 loads and processes one tile at a
 // time; DEPTH = D >= 1 keeps the loads of the next D tiles in flight while
 // a tile is processed (a ring of D register buffers, indexed at compile
 // time by unrolling).
-template <int DEPTH, class Tile, class Load, class Proc>
+template <int DEPTH, int WPB, class Tile, class Load, class Proc>
 SDP4_DEV void tile_loop(int64_t ntiles, Load load, Proc proc)
 {
     const int wave = threadIdx.x / kWave;
-    const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
-    int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+    const int64_t stride = (int64_t)gridDim.x * WPB;
+    int64_t t = (int64_t)blockIdx.x * WPB + wave;
     if constexpr (DEPTH == 0) {
         for (; t < ntiles; t += stride) {
             Tile in;
@@ -117,17 +135,18 @@ SDP4_DEV void maybe_fwht(float (&v)[E], float cn)
 // (codes 0..15, scale and minimum) or, with SYM, symmetric (codes -7..7,
 // scale only; minv is not touched)
 // ---------------------------------------------------------------------------
-template <bool BF16, bool SYM, int E, int DEPTH>
-__global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
+template <bool BF16, bool SYM, int E, int DEPTH, int WPB>
+__global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     const float *__restrict__ w_new, const void *__restrict__ w_prev, int64_t n, int group,
     uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv)
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;                       // f32 chunks per lane
     constexpr int RP = BF16 ? E / 8 : E / 4;       // previous-weight chunks per lane
-    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    __shared__ u32x4 lds_all[WPB][kWave * R];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
+    const int gs = group_shift(group);
     const int lanes_per_group = group / E;
     struct Tile {
         u32x4 a[R];
@@ -178,8 +197,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
             for (int i = 0; i < E; ++i)
                 q[i] = code_bits(d[i], inv);
             store_codes<E, 4>(codes + base / 2, valid, lds, q);
-            if (off < valid && off % group == 0)
-                scale[(base + off) / group] = s;
+            if (off < valid && (off & (group - 1)) == 0)
+                scale[(base + off) >> gs] = s;
             return;
         }
         float mn = d[0], mx = d[0];
@@ -199,13 +218,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
         for (int i = 0; i < E; ++i)
             q[i] = code_bits(d[i] - mn, inv);
         store_codes<E, 4>(codes + base / 2, valid, lds, q);
-        if (off < valid && off % group == 0) {
-            const int64_t gi = (base + off) / group;
+        if (off < valid && (off & (group - 1)) == 0) {
+            const int64_t gi = (base + off) >> gs;
             scale[gi] = s;
             minv[gi] = mn;
         }
     };
-    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, WPB, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
@@ -213,16 +232,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_encode(
 // fma(code, scale, min), or with SYM value = code * scale (signed codes,
 // minv not read)
 // ---------------------------------------------------------------------------
-template <bool BF16, bool SYM, int E, int DEPTH>
-__global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
+template <bool BF16, bool SYM, int E, int DEPTH, int WPB>
+__global__ __launch_bounds__(kWave * WPB) void k_qwd_decode(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const float *__restrict__ minv, int64_t n, int group, void *__restrict__ w_prev)
 {
     constexpr int W = kWave * E;
     constexpr int RP = BF16 ? E / 8 : E / 4;
-    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * (E / 4)];
+    __shared__ u32x4 lds_all[WPB][kWave * (E / 4)];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
+    const int gs = group_shift(group);
     struct Tile {
         u32x4 c[E / 32];
         float s, mn;
@@ -237,7 +257,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
 #pragma unroll
             for (int k = 0; k < E / 32; ++k)
                 in.c[k] = __builtin_nontemporal_load(src + k);
-            const int64_t gi = (base + off) / group;
+            const int64_t gi = (base + off) >> gs;
             in.s = scale[gi];
             in.mn = SYM ? 0.0f : minv[gi];
         } else {
@@ -284,23 +304,24 @@ __global__ __launch_bounds__(kBlockThreads) void k_qwd_decode(
             stage_out<RP>(reinterpret_cast<u32x4 *>(static_cast<float *>(w_prev) + base), valid / 4, lds, c);
         }
     };
-    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, WPB, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
 // K1: blockwise Hadamard (block NB, 0 = none) + symmetric BITS-bit group quantization
 // ---------------------------------------------------------------------------
-template <int BITS, int E, int NB, int DEPTH, bool SR = false>
-__global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
+template <int BITS, int E, int NB, int DEPTH, int WPB, bool SR = false>
+__global__ __launch_bounds__(kWave * WPB) void k_grad_quant(
     const float *__restrict__ x, int64_t n, int group, float cn, uint8_t *__restrict__ codes,
     float *__restrict__ scale, uint64_t seed = 0, uint64_t offset = 0)
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;
     constexpr float qmax = BITS == 8 ? 127.0f : 7.0f;
-    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    __shared__ u32x4 lds_all[WPB][kWave * R];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
+    const int gs = group_shift(group);
     const int lanes_per_group = group / E;
     struct Tile {
         u32x4 a[R];
@@ -340,10 +361,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
         }
         store_codes<E, BITS>(codes + base * BITS / 8, valid, lds, q);
         const int off = E * lane;
-        if (off < valid && off % group == 0)
-            scale[(base + off) / group] = s;
+        if (off < valid && (off & (group - 1)) == 0)
+            scale[(base + off) >> gs] = s;
     };
-    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, WPB, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
@@ -351,17 +372,18 @@ __global__ __launch_bounds__(kBlockThreads) void k_grad_quant(
 // (BITS_OUT 4/8) or inverse Hadamard (block NB) + out_scale to float32
 // (BITS_OUT 0)
 // ---------------------------------------------------------------------------
-template <int BITS_IN, int BITS_OUT, int E, int NB, int PMAX, int DEPTH, bool SR = false>
-__global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
+template <int BITS_IN, int BITS_OUT, int E, int NB, int PMAX, int DEPTH, int WPB, bool SR = false>
+__global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
     PeerTable peers, int P, int64_t n, int group, float cn, float out_scale, uint8_t *__restrict__ out_codes,
     float *__restrict__ out_scales, float *__restrict__ out_f32, uint64_t seed = 0, uint64_t offset = 0)
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;
     constexpr int CW = E * BITS_IN / 128; // input chunks (16 B) per lane per peer
-    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    __shared__ u32x4 lds_all[WPB][kWave * R];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
+    const int gs = group_shift(group);
     struct Tile {
         u32x4 c[PMAX][CW];
         float s[PMAX];
@@ -370,7 +392,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
         const int64_t base = t * W;
         const int off = E * lane;
         const bool active = off < tile_valid(n, base, W);
-        const int64_t gi = (base + off) / group;
+        const int64_t gi = (base + off) >> gs;
 #pragma unroll
         for (int j = 0; j < PMAX; ++j) {
             if constexpr (SDP4_PEER_LDS && CW > 1) {
@@ -465,22 +487,22 @@ __global__ __launch_bounds__(kBlockThreads) void k_dequant_reduce(
                     q[i] = code_bits(acc[i], inv);
             }
             store_codes<E, BITS_OUT>(out_codes + base * BITS_OUT / 8, valid, lds, q);
-            if (off < valid && off % group == 0)
-                out_scales[(base + off) / group] = s;
+            if (off < valid && (off & (group - 1)) == 0)
+                out_scales[(base + off) >> gs] = s;
         }
     };
-    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, WPB, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
 // standalone Hadamard (unfused variant); in place allowed
 // ---------------------------------------------------------------------------
-template <int E, int NB, int DEPTH>
-__global__ __launch_bounds__(kBlockThreads) void k_hadamard(const float *x, float *y, int64_t n, float cn)
+template <int E, int NB, int DEPTH, int WPB>
+__global__ __launch_bounds__(kWave * WPB) void k_hadamard(const float *x, float *y, int64_t n, float cn)
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;
-    __shared__ u32x4 lds_all[kWavesPerBlock][kWave * R];
+    __shared__ u32x4 lds_all[WPB][kWave * R];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     struct Tile {
         u32x4 a[R];
@@ -501,26 +523,28 @@ __global__ __launch_bounds__(kBlockThreads) void k_hadamard(const float *x, floa
         f32_to_chunks<E>(v, c);
         stage_out<R>(reinterpret_cast<u32x4 *>(y + base), tile_valid(n, base, W) / 4, lds, c);
     };
-    tile_loop<DEPTH, Tile>((n + W - 1) / W, load, proc);
+    tile_loop<DEPTH, WPB, Tile>((n + W - 1) / W, load, proc);
 }
 
 // ---------------------------------------------------------------------------
 // launch helpers shared by the .hip translation units
 // ---------------------------------------------------------------------------
-inline int64_t wave_blocks(int64_t n, int E)
+template <int WPB>
+int64_t wave_blocks(int64_t n, int E)
 {
     const int64_t W = (int64_t)kWave * E;
     const int64_t tiles = (n + W - 1) / W;
-    return (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+    return (tiles + WPB - 1) / WPB;
 }
 
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
+constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC;
+constexpr int kK1Waves = SDP4_K1_WAVES, kK1Cap = SDP4_K1_BPC;
 
 // 64 elements per lane: required for groups of 4096 (a group must fit one
 // wavefront), allowed (preferred_e == 64) for any group of at least 64 (a
 // lane slice must not straddle groups); otherwise 32.
 inline bool use_wide_lanes(int group, int preferred_e) { return group > 64 * 32 || (preferred_e == 64 && group >= 64); }
-static_assert(kBlockThreads == kLaunchThreads, "block size");
 
 // Hadamard block sizes the kernels are compiled for: 0 (none), 2 .. 1024.
 template <template <int> class F, typename... A>
@@ -553,14 +577,15 @@ int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, flo
               uint64_t offset = 0)
 {
     constexpr int pipe = BITS_OUT == 0 ? kDepth : 0;
+    constexpr int WPB = kWavesPerBlock;
     if (P <= 4)
-        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe, SR>, wave_blocks(n, E), kCap, s, peers, P,
-                      n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
+        return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe, WPB, SR>, wave_blocks<WPB>(n, E), kCap,
+                           s, peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
     if (P <= 8)
-        return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe, SR>, wave_blocks(n, E), kCap, s, peers, P,
-                      n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
-    return launch(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, 0, SR>, wave_blocks(n, E), kCap, s, peers, P, n,
-                  group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
+        return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe, WPB, SR>, wave_blocks<WPB>(n, E), kCap,
+                           s, peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
+    return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, 0, WPB, SR>, wave_blocks<WPB>(n, E), kCap, s,
+                       peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
 }
 
 } // namespace sdp4

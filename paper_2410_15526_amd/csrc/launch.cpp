@@ -14,7 +14,7 @@ std::unordered_map<const void *, int> g_occ; // kernel -> resident blocks per CU
 int g_cus[64];
 } // namespace
 
-int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, hipError_t &err)
+int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, int block_threads, hipError_t &err)
 {
     int dev = 0;
     err = hipGetDevice(&dev);
@@ -34,7 +34,7 @@ int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, hipError_
         auto it = g_occ.find(kernel);
         if (it == g_occ.end()) {
             int nb = 0;
-            err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, kLaunchThreads, 0);
+            err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, block_threads, 0);
             if (err != hipSuccess)
                 return 0;
             it = g_occ.emplace(kernel, nb > 0 ? nb : 1).first;

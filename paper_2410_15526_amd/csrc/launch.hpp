@@ -10,10 +10,6 @@
 namespace sdp4 {
 
 constexpr int kMaxPeers = 16;
-#ifndef SDP4_WAVES_PER_BLOCK
-#define SDP4_WAVES_PER_BLOCK 4
-#endif
-constexpr int kLaunchThreads = 64 * SDP4_WAVES_PER_BLOCK;
 
 // Pointer tables passed by value in the kernel arguments.
 struct PeerTable {
@@ -27,16 +23,18 @@ struct F32Table {
 // Records `err` as the calling thread's last HIP error and returns SDP4_EHIP.
 int set_hip_error(hipError_t err);
 
-// Grid of a persistent kernel: the blocks of `kernel` that are resident at
-// once on the current device (capped at per_cu_cap per compute unit when
-// per_cu_cap > 0), and never more than nwork_blocks.
-int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, hipError_t &err);
+// Grid of a persistent kernel: the blocks of `kernel` (block_threads
+// threads each) that are resident at once on the current device (capped at
+// per_cu_cap per compute unit when per_cu_cap > 0), and never more than
+// nwork_blocks.
+int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, int block_threads, hipError_t &err);
 
-template <typename... Params, typename... Args>
+// Launch `kernel` with blocks of WAVES wavefronts.
+template <int WAVES, typename... Params, typename... Args>
 int launch(void (*kernel)(Params...), int64_t nwork_blocks, int per_cu_cap, hipStream_t stream, Args... args)
 {
     hipError_t err;
-    const int grid = grid_for(reinterpret_cast<const void *>(kernel), nwork_blocks, per_cu_cap, err);
+    const int grid = grid_for(reinterpret_cast<const void *>(kernel), nwork_blocks, per_cu_cap, 64 * WAVES, err);
     if (err != hipSuccess)
         return set_hip_error(err);
     std::tuple<Params...> values(args...);
@@ -45,7 +43,7 @@ int launch(void (*kernel)(Params...), int64_t nwork_blocks, int per_cu_cap, hipS
         int i = 0;
         ((argv[i++] = static_cast<void *>(&v)), ...);
     }, values);
-    err = hipLaunchKernel(reinterpret_cast<const void *>(kernel), dim3(grid), dim3(kLaunchThreads), argv, 0,
+    err = hipLaunchKernel(reinterpret_cast<const void *>(kernel), dim3(grid), dim3(64 * WAVES), argv, 0,
                           stream);
     if (err != hipSuccess)
         return set_hip_error(err);
