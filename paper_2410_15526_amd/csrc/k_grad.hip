@@ -11,13 +11,18 @@ struct GradQuant {
     static int run(const float *x, int64_t n, int bits, int group, float cn, uint8_t *codes, float *scale,
                    hipStream_t s)
     {
-        if (use_wide_lanes(group, SDP4_E_K1)) {   // 64 elements per lane: the default shape's register budget
+        if (use_wide_lanes(group, 32)) {   // 64 elements per lane: the default shape's register budget
             constexpr int WPB = kWavesPerBlock;
             auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth, WPB> : k_grad_quant<4, 64, NB, kDepth, WPB>;
             return launch<WPB>(k, wave_blocks<WPB>(n, 64), kCap, s, x, n, group, cn, codes, scale, uint64_t(0),
                                uint64_t(0));
         }
-        constexpr int WPB = kK1Waves;
+        if (bits == 8 && SDP4_E_K1 == 16 && group <= kWave * 16) {   // a group must fit one wavefront
+            constexpr int WPB = kK1Waves;
+            return launch<WPB>(k_grad_quant<8, 16, NB, kDepth, WPB>, wave_blocks<WPB>(n, 16), kK1Cap, s, x, n, group, cn,
+                               codes, scale, uint64_t(0), uint64_t(0));
+        }
+        constexpr int WPB = kK1Waves32;
         auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth, WPB> : k_grad_quant<4, 32, NB, kDepth, WPB>;
         return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, uint64_t(0),
                            uint64_t(0));

@@ -11,12 +11,12 @@ struct GradQuantSR {
     static int run(const float *x, int64_t n, int bits, int group, float cn, uint64_t seed, uint64_t offset,
                    uint8_t *codes, float *scale, hipStream_t s)
     {
-        if (use_wide_lanes(group, SDP4_E_K1)) {   // 64 elements per lane: the default shape's register budget
+        if (use_wide_lanes(group, 32)) {   // 64 elements per lane: the default shape's register budget
             constexpr int WPB = kWavesPerBlock;
             auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth, WPB, true> : k_grad_quant<4, 64, NB, kDepth, WPB, true>;
             return launch<WPB>(k, wave_blocks<WPB>(n, 64), kCap, s, x, n, group, cn, codes, scale, seed, offset);
         }
-        constexpr int WPB = kK1Waves;
+        constexpr int WPB = kK1Waves32;
         auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth, WPB, true> : k_grad_quant<4, 32, NB, kDepth, WPB, true>;
         return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, seed, offset);
     }

@@ -14,7 +14,9 @@
 // the measured best on MI355X: one tile prefetched, 32 elements per lane,
 // int8 peer chunks transposed through LDS, and per kernel family a block
 // shape -- one resident block of four waves per CU for the qWD encoder, one
-// block of eight waves for K1, two blocks of four waves for the rest.  (How
+// block of twelve waves for the 8-bit K1 (16 elements per lane) and of eight
+// for the 4-bit and stochastically rounded K1, two blocks of four waves for
+// the rest.  (How
 // many bytes a CU keeps in flight, and how far compute spreads its requests
 // out, moves the mixed read/write bandwidth of HBM by several per cent.)
 #pragma once
@@ -28,7 +30,8 @@
 #ifndef SDP4_PEER_LDS
 #define SDP4_PEER_LDS 1 // int8 peer chunks: coalesced loads + LDS transpose
 #endif
-// Elements per lane of each kernel family (32 or 64; group 4096 always uses 64).
+// Elements per lane of each kernel family (32 or 64, and 16 for the 8-bit K1;
+// group 4096 always uses 64).
 #ifndef SDP4_E_ENC
 #define SDP4_E_ENC 32
 #endif
@@ -36,7 +39,7 @@
 #define SDP4_E_DEC 32
 #endif
 #ifndef SDP4_E_K1
-#define SDP4_E_K1 32
+#define SDP4_E_K1 16 // 8-bit K1 only: 4-bit codes need 32 per lane to fill a 16-byte store
 #endif
 #ifndef SDP4_E_RED
 #define SDP4_E_RED 32
@@ -54,7 +57,10 @@
 #define SDP4_ENC_BPC 1
 #endif
 #ifndef SDP4_K1_WAVES
-#define SDP4_K1_WAVES 8
+#define SDP4_K1_WAVES 12 // K1 with 16 elements per lane
+#endif
+#ifndef SDP4_K1_WAVES_32
+#define SDP4_K1_WAVES_32 8 // K1 with 32 elements per lane (4-bit codes, stochastic rounding)
 #endif
 #ifndef SDP4_K1_BPC
 #define SDP4_K1_BPC 1
@@ -539,7 +545,7 @@ int64_t wave_blocks(int64_t n, int E)
 
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
 constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC;
-constexpr int kK1Waves = SDP4_K1_WAVES, kK1Cap = SDP4_K1_BPC;
+constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
 
 // 64 elements per lane: required for groups of 4096 (a group must fit one
 // wavefront), allowed (preferred_e == 64) for any group of at least 64 (a
