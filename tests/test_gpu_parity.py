@@ -49,7 +49,7 @@ def run_grad_quant(x: np.ndarray, bits, block, group):
 
 @pytest.mark.parametrize("bits", [8, 4])
 @pytest.mark.parametrize("block", [0, 2, 4, 16, 32, 64, 128, 256, 512, 1024])
-@pytest.mark.parametrize("group", [32, 64, 128, 256, 512, 2048, 4096])
+@pytest.mark.parametrize("group", [32, 64, 128, 256, 512, 1024, 2048, 4096])
 def test_grad_quant(bits, block, group):
     n = size_for(max(group, block))
     say(f"grad_quant bits={bits} block={block} group={group} n={n}")
