@@ -26,9 +26,10 @@
  *  Errors     Arguments are checked on the host before anything is
  *             enqueued; on any error nothing is written and nothing is
  *             launched.  Device faults surface at the caller's next sync.
- *  Sizes      n / n_chunk count elements and may be 0 (no-op).  They must be
- *             multiples of lcm(group, hadamard_block), which for the allowed
- *             powers of two is max(group, hadamard_block).
+ *  Sizes      n / n_chunk count elements and may be 0 (no-op), at most
+ *             SDP4_MAX_ELEMENTS.  They must be multiples of
+ *             lcm(group, hadamard_block), which for the allowed powers of
+ *             two is max(group, hadamard_block).
  *  Alignment  Element arrays (float data, codes) must be 16-byte aligned;
  *             per-group header arrays (scales, minima) 4-byte aligned.
  *  Aliasing   Outputs must not overlap inputs, except where stated.
@@ -40,7 +41,8 @@
  *  4-bit codes: two per byte, element 2j in the low nibble of byte j and
  *               element 2j+1 in the high nibble.  Gradient codes are signed
  *               two's-complement nibbles in [-7, 7]; weight-difference codes
- *               are unsigned in [0, 15].
+ *               are unsigned in [0, 15] (signed in [-7, 7] for the
+ *               symmetric qWD codec).
  *  Headers:     one float32 per group of `group` consecutive elements, in
  *               group order (scale; plus the group minimum for qWD).
  *  Chunk j of a message of n_chunk elements starts at byte
@@ -96,6 +98,7 @@ extern "C" {
 #define SDP4_MAX_GROUP 4096
 #define SDP4_MAX_HADAMARD 1024
 #define SDP4_MAX_PEERS 16
+#define SDP4_MAX_ELEMENTS ((int64_t)1 << 48) /* n above this is EINVAL (byte counts stay in range) */
 
 /*
  * qWD encode -- Alg. 2, CompressedForwardPass, first two steps: the weight

@@ -33,6 +33,7 @@ bool pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
 bool valid_group(int g) { return pow2(g) && g >= SDP4_MIN_GROUP && g <= SDP4_MAX_GROUP; }
 bool valid_block(int b) { return b == 0 || (pow2(b) && b >= 2 && b <= SDP4_MAX_HADAMARD); }
 bool valid_bits(int b) { return b == 4 || b == 8; }
+bool valid_n(int64_t n) { return n >= 0 && n <= SDP4_MAX_ELEMENTS; } // keeps byte counts far from overflow
 bool aligned(const void *p, std::uintptr_t a) { return reinterpret_cast<std::uintptr_t>(p) % a == 0; }
 
 // [a, a+na) and [b, b+nb) share a byte
@@ -97,7 +98,7 @@ int check_reduce_args(int P, const void *const *codes, const float *const *scale
 int qwd_encode(const float *w_new, const void *w_prev, int prev_dtype, int64_t n, int group,
                uint8_t *codes, float *scale, float *minv, bool sym, void *stream)
 {
-    if (n < 0 || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
+    if (!valid_n(n) || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
         return SDP4_EINVAL;
     if (n % group)
         return SDP4_EALIGN;
@@ -128,7 +129,7 @@ int qwd_encode(const float *w_new, const void *w_prev, int prev_dtype, int64_t n
 int qwd_decode(const uint8_t *codes, const float *scale, const float *minv, int64_t n, int group,
                void *w_prev, int prev_dtype, bool sym, void *stream)
 {
-    if (n < 0 || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
+    if (!valid_n(n) || !valid_group(group) || (prev_dtype != SDP4_F32 && prev_dtype != SDP4_BF16))
         return SDP4_EINVAL;
     if (n % group)
         return SDP4_EALIGN;
@@ -178,7 +179,7 @@ int sdp4_qwd_decode_sym(const uint8_t *codes, const float *scale, int64_t n, int
 int sdp4_grad_quant(const float *x, int64_t n, int bits, int hadamard_block, int group, void *codes,
                     float *scale, void *stream)
 {
-    if (n < 0 || !valid_bits(bits) || !valid_block(hadamard_block) || !valid_group(group))
+    if (!valid_n(n) || !valid_bits(bits) || !valid_block(hadamard_block) || !valid_group(group))
         return SDP4_EINVAL;
     if (n % lcm_pow2(group, hadamard_block))
         return SDP4_EALIGN;
@@ -198,7 +199,7 @@ int sdp4_grad_quant(const float *x, int64_t n, int bits, int hadamard_block, int
 int sdp4_grad_quant_sr(const float *x, int64_t n, int bits, int hadamard_block, int group, uint64_t seed,
                        uint64_t offset, void *codes, float *scale, void *stream)
 {
-    if (n < 0 || !valid_bits(bits) || !valid_block(hadamard_block) || !valid_group(group))
+    if (!valid_n(n) || !valid_bits(bits) || !valid_block(hadamard_block) || !valid_group(group))
         return SDP4_EINVAL;
     if (n % lcm_pow2(group, hadamard_block) || offset % 8)
         return SDP4_EALIGN;
@@ -221,7 +222,7 @@ int sdp4_dequant_reduce_sr(int P, const void *const *codes, const float *const *
 {
     if (P < 1 || P > SDP4_MAX_PEERS)
         return SDP4_ERANGE;
-    if (n_chunk < 0 || !valid_bits(bits_in) || !valid_group(group) || !valid_bits(bits_out))
+    if (!valid_n(n_chunk) || !valid_bits(bits_in) || !valid_group(group) || !valid_bits(bits_out))
         return SDP4_EINVAL;
     if (n_chunk % group || offset % 8)
         return SDP4_EALIGN;
@@ -244,7 +245,7 @@ int sdp4_dequant_reduce(int P, const void *const *codes, const float *const *sca
 {
     if (P < 1 || P > SDP4_MAX_PEERS)
         return SDP4_ERANGE;
-    if (n_chunk < 0 || !valid_bits(bits_in) || !valid_group(group) || !valid_block(hadamard_block) ||
+    if (!valid_n(n_chunk) || !valid_bits(bits_in) || !valid_group(group) || !valid_block(hadamard_block) ||
         !(bits_out == 0 || valid_bits(bits_out)) || !std::isfinite(out_scale))
         return SDP4_EINVAL;
     if (bits_out != 0 && hadamard_block != 0)
@@ -266,7 +267,7 @@ int sdp4_dequant_reduce(int P, const void *const *codes, const float *const *sca
 
 int sdp4_hadamard(const float *x, float *y, int64_t n, int block, void *stream)
 {
-    if (n < 0 || block == 0 || !valid_block(block))
+    if (!valid_n(n) || block == 0 || !valid_block(block))
         return SDP4_EINVAL;
     if (n % block)
         return SDP4_EALIGN;
@@ -285,7 +286,7 @@ int sdp4_reduce_f32(int P, const float *const *xs, float *y, int64_t n, void *st
 {
     if (P < 1 || P > SDP4_MAX_PEERS)
         return SDP4_ERANGE;
-    if (n < 0)
+    if (!valid_n(n))
         return SDP4_EINVAL;
     if (n == 0)
         return SDP4_OK;
@@ -308,7 +309,7 @@ int sdp4_reduce_f32(int P, const float *const *xs, float *y, int64_t n, void *st
 
 int sdp4_copy_f32(const float *x, float *y, int64_t n, void *stream)
 {
-    if (n < 0)
+    if (!valid_n(n))
         return SDP4_EINVAL;
     if (n == 0)
         return SDP4_OK;
@@ -323,14 +324,14 @@ int sdp4_copy_f32(const float *x, float *y, int64_t n, void *stream)
 
 int64_t sdp4_codes_bytes(int64_t n, int bits)
 {
-    if (n < 0 || !valid_bits(bits))
+    if (!valid_n(n) || !valid_bits(bits))
         return -1;
     return n * bits / 8;
 }
 
 int64_t sdp4_num_groups(int64_t n, int group)
 {
-    if (n < 0 || !valid_group(group))
+    if (!valid_n(n) || !valid_group(group))
         return -1;
     return n / group;
 }

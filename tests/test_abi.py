@@ -179,6 +179,20 @@ def test_hadamard_reduce_copy_validation():
     assert L.sdp4_copy_f32(A, B, 0, None) == OK
 
 
+def test_element_counts_beyond_the_limit_are_rejected():
+    big = (1 << 48) + 4096
+    L = sdp4.lib()
+    assert gq(n=big) == EINVAL and gq(n=1 << 62) == EINVAL
+    assert enc(n=big) == EINVAL and dec(n=big) == EINVAL
+    assert enc_sym(n=big) == EINVAL and dec_sym(n=big) == EINVAL
+    assert dr(n=big) == EINVAL
+    assert L.sdp4_grad_quant_sr(A, big, 8, 256, 128, 1, 0, B, CC, None) == EINVAL
+    assert L.sdp4_hadamard(A, B, big, 256, None) == EINVAL
+    assert L.sdp4_copy_f32(A, B, big, None) == EINVAL
+    assert L.sdp4_codes_bytes(big, 8) == -1 and L.sdp4_num_groups(big, 128) == -1
+    assert L.sdp4_codes_bytes(1 << 48, 8) == 1 << 48
+
+
 def test_binding_refuses_host_tensors():
     torch = pytest.importorskip("torch")
     x = torch.zeros(4096)
