@@ -99,10 +99,20 @@ SDP4_DEV int swz(int c)
 
 // Coalesced global loads of one tile: instruction i, lane l reads chunk
 // 64*i + l.  Chunks at or beyond `valid` are not read and are zero.
-template <int R>
+// WHOLE_FAST: a whole tile (every tile but the last) is loaded without
+// per-chunk guards.  Callers that batch the loads of several buffers (the
+// peers of a dequantize-reduce) keep the guarded form, whose loads the
+// compiler schedules together.
+template <int R, bool WHOLE_FAST = true>
 SDP4_DEV void gload(const u32x4 *__restrict__ g, int valid, u32x4 (&t)[R])
 {
     const int lane = lane_id();
+    if (WHOLE_FAST && valid >= kWave * R) {
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            t[i] = __builtin_nontemporal_load(g + kWave * i + lane);
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < R; ++i) {
         const int c = kWave * i + lane;
@@ -145,12 +155,20 @@ SDP4_DEV void stage_out(u32x4 *__restrict__ g, int valid, u32x4 *lds, const u32x
     for (int k = 0; k < R; ++k)
         lds[swz<R>(R * lane + k)] = in[k];
     wave_lds_sync();
+    if (valid >= kWave * R) {
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-        const int c = kWave * i + lane;
-        const u32x4 t = lds[swz<R>(c)];
-        if (c < valid)
-            __builtin_nontemporal_store(t, g + c);
+        for (int i = 0; i < R; ++i) {
+            const int c = kWave * i + lane;
+            __builtin_nontemporal_store(lds[swz<R>(c)], g + c);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const int c = kWave * i + lane;
+            const u32x4 t = lds[swz<R>(c)];
+            if (c < valid)
+                __builtin_nontemporal_store(t, g + c);
+        }
     }
     wave_lds_sync();
 }

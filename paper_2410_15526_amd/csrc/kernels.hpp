@@ -403,7 +403,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
         for (int j = 0; j < PMAX; ++j) {
             if constexpr (SDP4_PEER_LDS && CW > 1) {
                 if (j < P) {
-                    gload<CW>(reinterpret_cast<const u32x4 *>(static_cast<const uint8_t *>(peers.codes[j]) +
+                    gload<CW, false>(reinterpret_cast<const u32x4 *>(static_cast<const uint8_t *>(peers.codes[j]) +
                                                                base * BITS_IN / 8),
                               tile_valid(n, base, W) * BITS_IN / 128, in.c[j]);
                     in.s[j] = active ? peers.scales[j][gi] : 0.0f;
