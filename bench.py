@@ -66,9 +66,10 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_for(kernel: str):
+def traffic_for(kernel: str, workload: str = "c5"):
     """HBM traffic per launch from the committed rocprofv3 counter summary,
-    or None when that summary is missing or was taken on other kernel sources."""
+    or None when that summary is missing, was taken on other kernel sources,
+    or on another workload."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     if not os.path.exists(path):
         return None
@@ -76,7 +77,7 @@ def traffic_for(kernel: str):
         d = json.load(open(path))
     except ValueError:
         return None
-    if d.get("source_digest") != source_digest():
+    if d.get("source_digest") != source_digest() or d.get("workload_key", "c5") != workload:
         return None
     k = d.get("kernels", {}).get(kernel)
     return None if k is None else k.get("bytes_per_launch")
@@ -260,7 +261,7 @@ def main():
             table5[f"{mb}MB"] = row
             del x, c, s, y
 
-    traffic = traffic_for(dom)
+    traffic = traffic_for(dom, args.workload)
     line = {
         "metric": METRIC,
         "value": round(value, 1),
