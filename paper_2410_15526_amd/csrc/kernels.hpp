@@ -11,14 +11,14 @@
 // results do not depend on the grid size or on the prefetching.
 //
 // The SDP4_* macros below are build-time tuning knobs; their defaults are
-// the measured best on MI355X: one tile prefetched, 32 elements per lane,
-// int8 peer chunks transposed through LDS, and per kernel family a block
-// shape -- one resident block of four waves per CU for the qWD encoder, one
-// block of twelve waves for the 8-bit K1 (16 elements per lane) and of eight
-// for the 4-bit and stochastically rounded K1, two blocks of four waves for
-// the rest.  (How
-// many bytes a CU keeps in flight, and how far compute spreads its requests
-// out, moves the mixed read/write bandwidth of HBM by several per cent.)
+// the measured best on MI355X: one tile prefetched, 32 elements per lane
+// (16 for the 8-bit K1), int8 peer chunks transposed through LDS, and per
+// kernel family a block shape -- one resident block of four waves per CU
+// for the qWD encoder, one block of twelve waves for the 8-bit K1 and of
+// eight for the 4-bit and stochastically rounded K1, two blocks of four
+// waves for the rest.  (How many bytes a CU keeps in flight, and how far
+// compute spreads its requests out, moves the mixed read/write bandwidth of
+// HBM by several per cent.)
 #pragma once
 
 #include "device.hpp"
@@ -71,10 +71,10 @@ namespace sdp4 {
 constexpr int kDepth = SDP4_PIPE;
 
 // Persistent loop of one wavefront over its tiles t, t + S, t + 2S, ...
-// (S = waves in the grid, WPB waves per block).  DEPTH = 0 loads and processes one tile at a
-// time; DEPTH = D >= 1 keeps the loads of the next D tiles in flight while
-// a tile is processed (a ring of D register buffers, indexed at compile
-// time by unrolling).
+// (S = waves in the grid, WPB waves per block).  DEPTH = 0 loads and
+// processes one tile at a time; DEPTH = D >= 1 keeps the loads of the next
+// D tiles in flight while a tile is processed (a ring of D register
+// buffers, indexed at compile time by unrolling).
 template <int DEPTH, int WPB, class Tile, class Load, class Proc>
 SDP4_DEV void tile_loop(int64_t ntiles, Load load, Proc proc)
 {
@@ -403,9 +403,9 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
         for (int j = 0; j < PMAX; ++j) {
             if constexpr (SDP4_PEER_LDS && CW > 1) {
                 if (j < P) {
-                    gload<CW, false>(reinterpret_cast<const u32x4 *>(static_cast<const uint8_t *>(peers.codes[j]) +
-                                                               base * BITS_IN / 8),
-                              tile_valid(n, base, W) * BITS_IN / 128, in.c[j]);
+                    const auto *src = static_cast<const uint8_t *>(peers.codes[j]) + base * BITS_IN / 8;
+                    gload<CW, false>(reinterpret_cast<const u32x4 *>(src), tile_valid(n, base, W) * BITS_IN / 128,
+                                     in.c[j]);
                     in.s[j] = active ? peers.scales[j][gi] : 0.0f;
                 }
                 continue;
