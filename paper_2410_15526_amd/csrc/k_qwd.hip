@@ -13,7 +13,19 @@ int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, in
     constexpr int WPB = kEncWaves;
     auto k = bf16 ? (sym ? k_qwd_encode<true, true, E, kDepth, WPB> : k_qwd_encode<true, false, E, kDepth, WPB>)
                   : (sym ? k_qwd_encode<false, true, E, kDepth, WPB> : k_qwd_encode<false, false, E, kDepth, WPB>);
-    return launch<WPB>(k, wave_blocks<WPB>(n, E), kEncCap, s, w_new, w_prev, n, group, codes, scale, minv);
+    // Read/write phases for large launches with 32 elements per lane and a
+    // group of at least kEncPhaseMinGroup; everything else streams as usual.
+    uint64_t period = 0, read_ticks = 0;
+    if (E == 32 && SDP4_ENC_PHASE_US > 0 && n >= kPhaseMinElements && group >= kEncPhaseMinGroup) {
+        hipError_t err;
+        const int khz = wall_clock_khz(err);
+        if (err != hipSuccess)
+            return set_hip_error(err);
+        period = (uint64_t)khz * SDP4_ENC_PHASE_US / 1000;
+        read_ticks = period * SDP4_ENC_READ_PCT / 100;
+    }
+    return launch<WPB>(k, wave_blocks<WPB>(n, E), kEncCap, s, w_new, w_prev, n, group, codes, scale, minv, period,
+                       read_ticks);
 }
 
 template <int E>

@@ -66,9 +66,19 @@
 #define SDP4_K1_BPC 1
 #endif
 
+#ifndef SDP4_ENC_PHASE_US
+#define SDP4_ENC_PHASE_US 44 // qWD encoder read/write period in microseconds (0: ordinary stream)
+#endif
+#ifndef SDP4_ENC_READ_PCT
+#define SDP4_ENC_READ_PCT 90 // per cent of the period spent reading
+#endif
+
 namespace sdp4 {
 
 constexpr int kDepth = SDP4_PIPE;
+constexpr int kEncPhaseCap = 24;            // tiles buffered per wave by the phased encoder
+constexpr int kEncPhaseMinGroup = 128;      // smallest group the phased encoder buffers headers for
+constexpr int64_t kPhaseMinElements = 1 << 26; // smaller launches use the ordinary stream
 
 // Persistent loop of one wavefront over its tiles t, t + S, t + 2S, ...
 // (S = waves in the grid, WPB waves per block).  DEPTH = 0 loads and
@@ -109,6 +119,49 @@ SDP4_DEV void tile_loop(int64_t ntiles, Load load, Proc proc)
 
 SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base < W ? n - base : W); }
 
+// HBM serves a pure read stream or a pure write stream faster than a mix of
+// the two, and every CU reads the same constant-rate wall clock.  In a
+// phased loop all waves of the chip issue loads only while
+// (clock mod period) < read_ticks and keep each tile's (small) output in a
+// wave-private LDS buffer of up to `cap` tiles, which they write out in the
+// rest of the period -- so the memory system sees long read-only and
+// write-only stretches instead of a mix.  proc(t, in, slot) computes tile t
+// into buffer slot `slot`; flush(k) writes slots 0..k-1.  One tile is
+// prefetched.  Every wait is a short sleep until the clock moves to the
+// other phase, and the loop ends once the wave has no tile left and an
+// empty buffer, so every wave exits.  Results do not depend on the timing.
+template <int WPB, class Tile, class Load, class Proc, class Flush>
+SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_t read_ticks, Load load, Proc proc,
+                               Flush flush)
+{
+    const int wave = threadIdx.x / kWave;
+    const int64_t stride = (int64_t)gridDim.x * WPB;
+    int64_t t = (int64_t)blockIdx.x * WPB + wave;
+    Tile in;
+    bool have = t < ntiles;
+    if (have)
+        load(t, in);
+    int nbuf = 0;
+    for (;;) {
+        const bool reading = (uint64_t)wall_clock64() % period < read_ticks;
+        if (have && nbuf < cap && reading) {
+            proc(t, in, nbuf);
+            ++nbuf;
+            t += stride;
+            have = t < ntiles;
+            if (have)
+                load(t, in);
+        } else if (nbuf > 0 && (!reading || !have)) {
+            flush(nbuf);
+            nbuf = 0;
+        } else if (!have) {
+            break; // no tile left and the buffer is empty
+        } else {
+            __builtin_amdgcn_s_sleep(1); // buffer full in a read phase, or empty in a write phase
+        }
+    }
+}
+
 // Store the packed codes of a tile (lane l owns bytes [l*E*BITS/8, ...)):
 // one 16-byte chunk per lane goes out directly; more go through the wave's
 // LDS region so that every store instruction writes 1 KiB contiguous.
@@ -144,16 +197,27 @@ SDP4_DEV void maybe_fwht(float (&v)[E], float cn)
 template <bool BF16, bool SYM, int E, int DEPTH, int WPB>
 __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     const float *__restrict__ w_new, const void *__restrict__ w_prev, int64_t n, int group,
-    uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv)
+    uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv, uint64_t period,
+    uint64_t read_ticks)
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;                       // f32 chunks per lane
     constexpr int RP = BF16 ? E / 8 : E / 4;       // previous-weight chunks per lane
+    // Phased mode (E = 32: one 16-byte code chunk per lane and tile) buffers
+    // CAP tiles per wave: codes, then scales and minima of up to HMAX groups.
+    constexpr bool PHASED = E == 32;
+    constexpr int CAP = PHASED ? kEncPhaseCap : 1;
+    constexpr int HMAX = W / kEncPhaseMinGroup;
     __shared__ u32x4 lds_all[WPB][kWave * R];
-    u32x4 *lds = lds_all[threadIdx.x / kWave];
+    __shared__ u32x4 cbuf_all[WPB][CAP * kWave];
+    __shared__ float hbuf_all[WPB][CAP * 2 * HMAX];
+    __shared__ int64_t tbuf_all[WPB][CAP];
+    const int wv = threadIdx.x / kWave;
+    u32x4 *lds = lds_all[wv];
     const int lane = lane_id();
     const int gs = group_shift(group);
     const int lanes_per_group = group / E;
+    const int off = E * lane;
     struct Tile {
         u32x4 a[R];
         u32x4 b[RP];
@@ -169,9 +233,9 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
             gload<RP>(reinterpret_cast<const u32x4 *>(static_cast<const float *>(w_prev) + base), valid / 4,
                       in.b);
     };
-    auto proc = [&](int64_t t, Tile &in) {
-        const int64_t base = t * W;
-        const int valid = tile_valid(n, base, W);
+    // d = w_new - widen(w_prev), the group parameters (scale s, minimum mn;
+    // SYM: mn = 0, unused) and the code bits of this lane's E elements.
+    auto quantize = [&](Tile &in, uint32_t (&q)[E], float &s, float &mn) {
         float d[E], p[E];
         {
             u32x4 c[R];
@@ -189,48 +253,95 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
 #pragma unroll
         for (int i = 0; i < E; ++i)
             d[i] = d[i] - p[i];
-        const int off = E * lane;
         if constexpr (SYM) {
             float a = 0.0f;
 #pragma unroll
             for (int i = 0; i < E; ++i)
                 a = fmaxf(a, fabsf(d[i]));
             max_lanes(a, lanes_per_group);
-            float s, inv;
+            float inv;
             sym_params(a, 7.0f, s, inv);
-            uint32_t q[E];
+            mn = 0.0f;
 #pragma unroll
             for (int i = 0; i < E; ++i)
                 q[i] = code_bits(d[i], inv);
-            store_codes<E, 4>(codes + base / 2, valid, lds, q);
-            if (off < valid && (off & (group - 1)) == 0)
-                scale[(base + off) >> gs] = s;
-            return;
-        }
-        float mn = d[0], mx = d[0];
+        } else {
+            mn = d[0];
+            float mx = d[0];
 #pragma unroll
-        for (int i = 1; i < E; ++i) {
-            mn = fminf(mn, d[i]);
-            mx = fmaxf(mx, d[i]);
-        }
-        minmax_lanes(mn, mx, lanes_per_group);
-        const float range = mx - mn;
-        const float r = 15.0f / range;
-        const bool degenerate = !(range > 0.0f) || !__builtin_isfinite(range) || !__builtin_isfinite(r);
-        const float s = degenerate ? 0.0f : range / 15.0f;
-        const float inv = degenerate ? 0.0f : r;
-        uint32_t q[E];
+            for (int i = 1; i < E; ++i) {
+                mn = fminf(mn, d[i]);
+                mx = fmaxf(mx, d[i]);
+            }
+            minmax_lanes(mn, mx, lanes_per_group);
+            const float range = mx - mn;
+            const float r = 15.0f / range;
+            const bool degenerate = !(range > 0.0f) || !__builtin_isfinite(range) || !__builtin_isfinite(r);
+            s = degenerate ? 0.0f : range / 15.0f;
+            const float inv = degenerate ? 0.0f : r;
 #pragma unroll
-        for (int i = 0; i < E; ++i)
-            q[i] = code_bits(d[i] - mn, inv);
-        store_codes<E, 4>(codes + base / 2, valid, lds, q);
-        if (off < valid && (off & (group - 1)) == 0) {
-            const int64_t gi = (base + off) >> gs;
-            scale[gi] = s;
-            minv[gi] = mn;
+            for (int i = 0; i < E; ++i)
+                q[i] = code_bits(d[i] - mn, inv);
         }
     };
-    tile_loop<DEPTH, WPB, Tile>((n + W - 1) / W, load, proc);
+    const int64_t ntiles = (n + W - 1) / W;
+    if (!PHASED || period == 0) { // ordinary stream: each tile's output is stored at once
+        auto proc = [&](int64_t t, Tile &in) {
+            const int64_t base = t * W;
+            const int valid = tile_valid(n, base, W);
+            uint32_t q[E];
+            float s, mn;
+            quantize(in, q, s, mn);
+            store_codes<E, 4>(codes + base / 2, valid, lds, q);
+            if (off < valid && (off & (group - 1)) == 0) {
+                const int64_t gi = (base + off) >> gs;
+                scale[gi] = s;
+                if constexpr (!SYM)
+                    minv[gi] = mn;
+            }
+        };
+        tile_loop<DEPTH, WPB, Tile>(ntiles, load, proc);
+        return;
+    }
+    if constexpr (PHASED) { // group >= kEncPhaseMinGroup (the launcher checks)
+        u32x4 *cbuf = cbuf_all[wv];
+        float *hbuf = hbuf_all[wv];
+        int64_t *tbuf = tbuf_all[wv];
+        auto proc = [&](int64_t t, Tile &in, int slot) {
+            uint32_t q[E];
+            float s, mn;
+            quantize(in, q, s, mn);
+            u32x4 pk[1];
+            pack4<E>(q, pk);
+            cbuf[slot * kWave + lane] = pk[0];
+            if ((off & (group - 1)) == 0) {
+                const int g = off >> gs; // group within the tile, < W / group <= HMAX
+                hbuf[slot * 2 * HMAX + g] = s;
+                hbuf[slot * 2 * HMAX + HMAX + g] = mn;
+            }
+            if (lane == 0)
+                tbuf[slot] = t;
+        };
+        auto flush = [&](int k) {
+            wave_lds_sync();
+            const int hl = W >> gs; // headers per tile
+            for (int j = 0; j < k; ++j) {
+                const int64_t base = tbuf[j] * W;
+                const int valid = tile_valid(n, base, W);
+                if (off < valid)
+                    __builtin_nontemporal_store(cbuf[j * kWave + lane],
+                                                reinterpret_cast<u32x4 *>(codes + base / 2) + lane);
+                if (lane < hl && (lane << gs) < valid) {
+                    const int64_t gi = (base >> gs) + lane;
+                    scale[gi] = hbuf[j * 2 * HMAX + lane];
+                    if constexpr (!SYM)
+                        minv[gi] = hbuf[j * 2 * HMAX + HMAX + lane];
+                }
+            }
+            wave_lds_sync();
+        };
+        phased_tile_loop<WPB, Tile>(ntiles, CAP, period, read_ticks, load, proc, flush);
+    }
 }
 
 // ---------------------------------------------------------------------------

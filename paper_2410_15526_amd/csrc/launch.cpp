@@ -12,7 +12,26 @@ namespace {
 std::mutex g_mu;
 std::unordered_map<const void *, int> g_occ; // kernel -> resident blocks per CU
 int g_cus[64];
+int g_khz[64];
 } // namespace
+
+int wall_clock_khz(hipError_t &err)
+{
+    int dev = 0;
+    err = hipGetDevice(&dev);
+    if (err != hipSuccess)
+        return 0;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (dev < 64 && g_khz[dev] != 0)
+        return g_khz[dev];
+    int v = 0;
+    err = hipDeviceGetAttribute(&v, hipDeviceAttributeWallClockRate, dev);
+    if (err != hipSuccess)
+        return 0;
+    if (dev < 64)
+        g_khz[dev] = v;
+    return v;
+}
 
 int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, int block_threads, hipError_t &err)
 {

@@ -29,6 +29,9 @@ int set_hip_error(hipError_t err);
 // nwork_blocks.
 int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, int block_threads, hipError_t &err);
 
+// Rate of the device's constant wall clock in kHz (cached per device).
+int wall_clock_khz(hipError_t &err);
+
 // Launch `kernel` with blocks of WAVES wavefronts.
 template <int WAVES, typename... Params, typename... Args>
 int launch(void (*kernel)(Params...), int64_t nwork_blocks, int per_cu_cap, hipStream_t stream, Args... args)

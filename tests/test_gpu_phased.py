@@ -1,0 +1,51 @@
+"""The qWD encoder's phased mode (large launches: loads only in the read part
+of a clock period, outputs buffered in LDS and written in the rest) against
+the oracle on every element: groups 128..1024, both codecs, float32 and
+bfloat16 model weights, and a shard whose last wave tile is partial."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_15526_amd import sdp4
+from tests._gpu import check_codes, check_headers, dev, empty, host, say, torch
+
+pytestmark = pytest.mark.gpu
+
+N = (1 << 26) + 3 * 1024          # above the phased-mode threshold; 3/2 tiles past a whole number
+
+
+def inputs(bf16, seed):
+    r = np.random.default_rng(seed)
+    base = (r.standard_normal(N) * 0.02).astype(np.float32)
+    if bf16:
+        prev = (base.view(np.uint32) >> 16).astype(np.uint16)
+        wide = (prev.astype(np.uint32) << 16).view(np.float32)
+    else:
+        prev, wide = base, base
+    new = (wide + (r.standard_t(3, N) * 5e-4).astype(np.float32)).astype(np.float32)
+    return new, prev
+
+
+@pytest.mark.parametrize("bf16,group", [(True, 128), (False, 256), (True, 512), (False, 1024)])
+def test_phased_asymmetric_encode_matches_oracle(bf16, group):
+    say(f"phased qwd encode bf16={bf16} group={group} n={N}")
+    new, prev = inputs(bf16, group)
+    codes, scale, minv = empty(N // 2, "u8"), empty(N // group, "f32"), empty(N // group, "f32")
+    sdp4.sdp4_qwd_encode(dev(new), dev(prev), group, codes, scale, minv)
+    torch().cuda.synchronize()
+    rc, rs, rm, pre = oracle.qwd_encode(new, prev, group)
+    check_headers(host(scale), rs)
+    check_headers(host(minv), rm, "minv")
+    check_codes(host(codes), rc, pre, N, 4, signed=False)
+
+
+@pytest.mark.parametrize("bf16,group", [(True, 128), (False, 512)])
+def test_phased_symmetric_encode_matches_oracle(bf16, group):
+    say(f"phased qwd encode sym bf16={bf16} group={group} n={N}")
+    new, prev = inputs(bf16, 7 * group)
+    codes, scale = empty(N // 2, "u8"), empty(N // group, "f32")
+    sdp4.sdp4_qwd_encode_sym(dev(new), dev(prev), group, codes, scale)
+    torch().cuda.synchronize()
+    rc, rs, pre = oracle.qwd_encode_sym(new, prev, group)
+    check_headers(host(scale), rs)
+    check_codes(host(codes), rc, pre, N, 4)
