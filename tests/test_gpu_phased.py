@@ -1,7 +1,8 @@
 """The qWD encoder's phased mode (large launches: loads only in the read part
 of a clock period, outputs buffered in LDS and written in the rest) against
 the oracle on every element: groups 128..1024, both codecs, float32 and
-bfloat16 model weights, and a shard whose last wave tile is partial."""
+bfloat16 model weights, and a shard whose last wave tile is partial.  The
+8-bit K1 is checked at the same size (it streams without phases)."""
 import numpy as np
 import pytest
 
@@ -49,3 +50,18 @@ def test_phased_symmetric_encode_matches_oracle(bf16, group):
     rc, rs, pre = oracle.qwd_encode_sym(new, prev, group)
     check_headers(host(scale), rs)
     check_codes(host(codes), rc, pre, N, 4)
+
+
+@pytest.mark.parametrize("block,group", [(256, 128), (0, 256), (32, 512), (1024, 1024)])
+def test_large_k1_matches_oracle(block, group):
+    """8-bit K1 (Hadamard + quantization) on a large shard, every element."""
+    say(f"large k1 block={block} group={group} n={N}")
+    r = np.random.default_rng(block + group)
+    x = (r.standard_normal(N) * 1e-4).astype(np.float32)
+    x[r.integers(0, N, N // 1000)] *= 100.0
+    codes, scale = empty(N, "u8"), empty(N // group, "f32")
+    sdp4.sdp4_grad_quant(dev(x), 8, block, group, codes, scale)
+    torch().cuda.synchronize()
+    rc, rs, pre = oracle.grad_quant(x, 8, block, group)
+    check_headers(host(scale), rs)
+    check_codes(host(codes), rc, pre, N, 8)
