@@ -129,7 +129,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU's share of the hot path; runs on more than one GPU are not "
-              "supported by this build (the collectives between the kernels are out of scope).",
+              "supported (the collectives between the kernels are not part of this library).",
               file=sys.stderr)
         sys.exit(2)
 

@@ -63,23 +63,49 @@ SDP4_DEV float xor_lane(float v)
     return __builtin_bit_cast(float, r);
 }
 
-SDP4_DEV void max_lanes(float &a, int lanes)
+// DPP exchanges inside rows of 16 lanes: quad_perm [1,0,3,2] (lane ^ 1),
+// quad_perm [2,3,0,1] (lane ^ 2), row_half_mirror (lane ^ 7 within 8 lanes),
+// row_ror:8 (lane ^ 8 within 16 lanes).  Every source lane is valid, so no
+// lane falls back to the `old` operand.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppRor8 = 0x128;
+
+template <int CTRL>
+SDP4_DEV uint32_t dpp_u32(uint32_t v)
 {
-    // reduce over `lanes` (power of two, 1..64) neighbouring lanes
-    if (lanes > 1) a = fmaxf(a, xor_lane<1>(a));
-    if (lanes > 2) a = fmaxf(a, xor_lane<2>(a));
-    if (lanes > 4) a = fmaxf(a, xor_lane<4>(a));
-    if (lanes > 8) a = fmaxf(a, xor_lane<8>(a));
-    if (lanes > 16) a = fmaxf(a, xor_lane<16>(a));
-    if (lanes > 32) a = fmaxf(a, xor_lane<32>(a));
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
 }
 
+template <int CTRL>
+SDP4_DEV float dpp_f32(float v)
+{
+    return __uint_as_float(dpp_u32<CTRL>(__float_as_uint(v)));
+}
+
+// Largest value over an aligned block of `lanes` (power of two, 1..64)
+// neighbouring lanes, for a >= +0 (a largest magnitude).  Non-negative
+// floats order like their bit patterns, so this is an unsigned maximum,
+// which the compiler fuses with the DPP exchange.  A maximum may join the
+// lanes of the block in any order: lane ^ 1, lane ^ 2, the mirror within 8
+// (lane ^ 7), lane ^ 8 within 16, then lane ^ 16 and lane ^ 32.
+SDP4_DEV void max_lanes(float &a, int lanes)
+{
+    uint32_t b = __float_as_uint(a);
+    if (lanes > 1) b = max(b, dpp_u32<kDppXor1>(b));
+    if (lanes > 2) b = max(b, dpp_u32<kDppXor2>(b));
+    if (lanes > 4) b = max(b, dpp_u32<kDppHalfMirror>(b));
+    if (lanes > 8) b = max(b, dpp_u32<kDppRor8>(b));
+    if (lanes > 16) b = max(b, (uint32_t)__builtin_amdgcn_ds_swizzle((int)b, (16 << 10) | 0x1F));
+    if (lanes > 32) b = max(b, (uint32_t)__builtin_amdgcn_ds_bpermute((lane_id() ^ 32) << 2, (int)b));
+    a = __uint_as_float(b);
+}
+
+// Smallest and largest value over an aligned block of `lanes` lanes.
 SDP4_DEV void minmax_lanes(float &mn, float &mx, int lanes)
 {
-    if (lanes > 1) { mn = fminf(mn, xor_lane<1>(mn)); mx = fmaxf(mx, xor_lane<1>(mx)); }
-    if (lanes > 2) { mn = fminf(mn, xor_lane<2>(mn)); mx = fmaxf(mx, xor_lane<2>(mx)); }
-    if (lanes > 4) { mn = fminf(mn, xor_lane<4>(mn)); mx = fmaxf(mx, xor_lane<4>(mx)); }
-    if (lanes > 8) { mn = fminf(mn, xor_lane<8>(mn)); mx = fmaxf(mx, xor_lane<8>(mx)); }
+    if (lanes > 1) { mn = fminf(mn, dpp_f32<kDppXor1>(mn)); mx = fmaxf(mx, dpp_f32<kDppXor1>(mx)); }
+    if (lanes > 2) { mn = fminf(mn, dpp_f32<kDppXor2>(mn)); mx = fmaxf(mx, dpp_f32<kDppXor2>(mx)); }
+    if (lanes > 4) { mn = fminf(mn, dpp_f32<kDppHalfMirror>(mn)); mx = fmaxf(mx, dpp_f32<kDppHalfMirror>(mx)); }
+    if (lanes > 8) { mn = fminf(mn, dpp_f32<kDppRor8>(mn)); mx = fmaxf(mx, dpp_f32<kDppRor8>(mx)); }
     if (lanes > 16) { mn = fminf(mn, xor_lane<16>(mn)); mx = fmaxf(mx, xor_lane<16>(mx)); }
     if (lanes > 32) { mn = fminf(mn, xor_lane<32>(mn)); mx = fmaxf(mx, xor_lane<32>(mx)); }
 }
@@ -120,10 +146,11 @@ SDP4_DEV void gload(const u32x4 *__restrict__ g, int valid, u32x4 (&t)[R])
     }
 }
 
-// Coalesced chunks -> lane-contiguous chunks (lane l gets chunks R*l .. R*l+R-1)
-// through the wave's LDS region.
+// Coalesced chunks -> lane-contiguous chunks through the wave's LDS region:
+// lane l gets the chunks R*el .. R*el+R-1 of element lane el (el = l unless
+// the kernel relabels its lanes, see element_lane).
 template <int R>
-SDP4_DEV void transpose_in(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R])
+SDP4_DEV void transpose_in(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R], int el)
 {
     const int lane = lane_id();
 #pragma unroll
@@ -132,8 +159,14 @@ SDP4_DEV void transpose_in(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R])
     wave_lds_sync();
 #pragma unroll
     for (int k = 0; k < R; ++k)
-        out[k] = lds[swz<R>(R * lane + k)];
+        out[k] = lds[swz<R>(R * el + k)];
     wave_lds_sync();
+}
+
+template <int R>
+SDP4_DEV void transpose_in(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R])
+{
+    transpose_in<R>(t, lds, out, lane_id());
 }
 
 // Global (coalesced) -> registers (lane-contiguous).
@@ -145,15 +178,15 @@ SDP4_DEV void stage_in(const u32x4 *__restrict__ g, int valid, u32x4 *lds, u32x4
     transpose_in<R>(t, lds, out);
 }
 
-// Registers (lane-contiguous) -> global (coalesced).  Chunks at or beyond
-// `valid` are not written.
+// Registers (lane-contiguous, element lane el) -> global (coalesced).
+// Chunks at or beyond `valid` are not written.
 template <int R>
-SDP4_DEV void stage_out(u32x4 *__restrict__ g, int valid, u32x4 *lds, const u32x4 (&in)[R])
+SDP4_DEV void stage_out(u32x4 *__restrict__ g, int valid, u32x4 *lds, const u32x4 (&in)[R], int el)
 {
     const int lane = lane_id();
 #pragma unroll
     for (int k = 0; k < R; ++k)
-        lds[swz<R>(R * lane + k)] = in[k];
+        lds[swz<R>(R * el + k)] = in[k];
     wave_lds_sync();
     if (valid >= kWave * R) {
 #pragma unroll
@@ -171,6 +204,12 @@ SDP4_DEV void stage_out(u32x4 *__restrict__ g, int valid, u32x4 *lds, const u32x
         }
     }
     wave_lds_sync();
+}
+
+template <int R>
+SDP4_DEV void stage_out(u32x4 *__restrict__ g, int valid, u32x4 *lds, const u32x4 (&in)[R])
+{
+    stage_out<R>(g, valid, lds, in, lane_id());
 }
 
 template <int E>
@@ -273,6 +312,100 @@ SDP4_DEV void fwht_lane(float (&v)[E], float cn)
 #pragma unroll
     for (int i = 0; i < E; ++i)
         v[i] = v[i] * cn;
+}
+
+// Relabeled lanes for the fused Hadamard kernels.  Inside each row of 16
+// lanes, physical lane p holds element lane el = p ^ (3 * p2) (bits 0 and 1
+// flipped when bit 2 is set; bits 2 and up unchanged; the map is its own
+// inverse).  Element-lane partners el ^ 1, el ^ 2, el ^ 4, el ^ 8 then sit at
+// physical lanes p ^ 1, p ^ 2, p ^ 7, p ^ 8, all reachable by DPP, and every
+// aligned block of 2^k lanes holds the same lanes as before, so group
+// reductions are unchanged.
+SDP4_DEV int element_lane(int p)
+{
+    const int b = (p >> 2) & 1;
+    return p ^ (b * 3);
+}
+
+// One cross-lane butterfly stage as a single v_fmac_f32_dpp per element:
+// v = v + sg * partner, sg = +1 in the lower lane (element-lane bit D clear)
+// and -1 in the upper one.  The upper lane thus holds b - a = -(a - b):
+// each lane carries its value up to a sign that depends only on the lane,
+// and since round-to-nearest-even is symmetric, fl(+-(a + b)) and
+// fl(+-(a - b)) are exactly the negated roundings.  (Values that carry a
+// sign flip and the matching partner signs always give sg = +-1 as above:
+// both lanes of a pair carry the same flip before the stage.)  The 16
+// instructions of a block start after 5 wait states, the longest DPP read
+// hazard (a VALU write of the source VGPR needs 2, of EXEC 5).
+#define SDP4_FMAC_DPP_I(i, CTRL) "v_fmac_f32_dpp %" #i ", %" #i ", %16 " CTRL " row_mask:0xf bank_mask:0xf\n\t"
+#define SDP4_FMAC_DPP_16(CTRL, w, s)                                                                             \
+    asm volatile("s_nop 4\n\t" SDP4_FMAC_DPP_I(0, CTRL) SDP4_FMAC_DPP_I(1, CTRL) SDP4_FMAC_DPP_I(2, CTRL)        \
+                     SDP4_FMAC_DPP_I(3, CTRL) SDP4_FMAC_DPP_I(4, CTRL) SDP4_FMAC_DPP_I(5, CTRL)                 \
+                         SDP4_FMAC_DPP_I(6, CTRL) SDP4_FMAC_DPP_I(7, CTRL) SDP4_FMAC_DPP_I(8, CTRL)             \
+                             SDP4_FMAC_DPP_I(9, CTRL) SDP4_FMAC_DPP_I(10, CTRL) SDP4_FMAC_DPP_I(11, CTRL)       \
+                                 SDP4_FMAC_DPP_I(12, CTRL) SDP4_FMAC_DPP_I(13, CTRL) SDP4_FMAC_DPP_I(14, CTRL)  \
+                                     SDP4_FMAC_DPP_I(15, CTRL)                                                  \
+                 : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]), "+v"(w[4]), "+v"(w[5]), "+v"(w[6]),         \
+                   "+v"(w[7]), "+v"(w[8]), "+v"(w[9]), "+v"(w[10]), "+v"(w[11]), "+v"(w[12]), "+v"(w[13]),      \
+                   "+v"(w[14]), "+v"(w[15])                                                                     \
+                 : "v"(s))
+
+template <int E, int D>
+SDP4_DEV void fwht_cross_signed(float (&v)[E], int el)
+{
+    static_assert(E % 16 == 0, "lane slice");
+    const float sg = (el & D) ? -1.0f : 1.0f;
+    if constexpr (D <= 8) {
+#pragma unroll
+        for (int b = 0; b < E / 16; ++b) {
+            float(&w)[16] = *reinterpret_cast<float(*)[16]>(v + 16 * b);
+            if constexpr (D == 1)
+                SDP4_FMAC_DPP_16("quad_perm:[1,0,3,2]", w, sg);
+            else if constexpr (D == 2)
+                SDP4_FMAC_DPP_16("quad_perm:[2,3,0,1]", w, sg);
+            else if constexpr (D == 4)
+                SDP4_FMAC_DPP_16("row_half_mirror", w, sg);
+            else
+                SDP4_FMAC_DPP_16("row_ror:8", w, sg);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+            v[i] = __builtin_fmaf(xor_lane<D>(v[i]), sg, v[i]);
+    }
+}
+
+// The blockwise transform of fwht_lane on relabeled lanes (element lane el):
+// the same stages in the same order with the same roundings, cross-lane
+// stages as fwht_cross_signed.  After the last stage a lane's values carry
+// the sign (-1)^popcount(el & (NB/E - 1)), which the final scaling by +-cn
+// removes; it is one fma with a +0 addend, so an exact zero comes out as +0
+// (the only difference from fwht_lane: -0 results become +0).
+template <int E, int NB>
+SDP4_DEV void fwht_lane_signed(float (&v)[E], float cn, int el)
+{
+    static_assert(NB > E && (NB & (NB - 1)) == 0 && NB <= 64 * E, "block");
+#pragma unroll
+    for (int h = 1; h < E; h <<= 1) {
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            if (i & h)
+                continue;
+            const float a = v[i], b = v[i + h];
+            v[i] = a + b;
+            v[i + h] = a - b;
+        }
+    }
+    fwht_cross_signed<E, 1>(v, el);
+    if constexpr (NB > 2 * E) fwht_cross_signed<E, 2>(v, el);
+    if constexpr (NB > 4 * E) fwht_cross_signed<E, 4>(v, el);
+    if constexpr (NB > 8 * E) fwht_cross_signed<E, 8>(v, el);
+    if constexpr (NB > 16 * E) fwht_cross_signed<E, 16>(v, el);
+    if constexpr (NB > 32 * E) fwht_cross_signed<E, 32>(v, el);
+    const float c = (__builtin_popcount(el & (NB / E - 1)) & 1) ? -cn : cn;
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+        v[i] = __builtin_fmaf(v[i], c, 0.0f);
 }
 
 // log2 of a group size (a power of two, checked on the host): header indices

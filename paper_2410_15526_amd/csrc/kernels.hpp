@@ -14,8 +14,7 @@
 // the measured best on MI355X: one tile prefetched, 32 elements per lane
 // (16 for the 8-bit K1), int8 peer chunks transposed through LDS, and per
 // kernel family a block shape -- one resident block of four waves per CU
-// for the qWD encoder, one block of twelve waves for the 8-bit K1 and of
-// eight for the 4-bit and stochastically rounded K1, two blocks of four
+// for the qWD encoder, one block of eight waves for K1, two blocks of four
 // waves for the rest.  (How many bytes a CU keeps in flight, and how far
 // compute spreads its requests out, moves the mixed read/write bandwidth of
 // HBM by several per cent.)
@@ -57,7 +56,7 @@
 #define SDP4_ENC_BPC 1
 #endif
 #ifndef SDP4_K1_WAVES
-#define SDP4_K1_WAVES 12 // K1 with 16 elements per lane
+#define SDP4_K1_WAVES 8 // K1 with 16 elements per lane
 #endif
 #ifndef SDP4_K1_WAVES_32
 #define SDP4_K1_WAVES_32 8 // K1 with 32 elements per lane (4-bit codes, stochastic rounding)
@@ -162,11 +161,12 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
     }
 }
 
-// Store the packed codes of a tile (lane l owns bytes [l*E*BITS/8, ...)):
-// one 16-byte chunk per lane goes out directly; more go through the wave's
-// LDS region so that every store instruction writes 1 KiB contiguous.
+// Store the packed codes of a tile (element lane el owns bytes
+// [el*E*BITS/8, ...)): one 16-byte chunk per lane goes out directly; more
+// go through the wave's LDS region so that every store instruction writes
+// 1 KiB contiguous.
 template <int E, int BITS>
-SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, const uint32_t (&q)[E])
+SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, const uint32_t (&q)[E], int el)
 {
     constexpr int RC = E * BITS / 128; // 16-byte chunks per lane
     u32x4 pk[RC];
@@ -175,11 +175,17 @@ SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, cons
     else
         pack4<E>(q, pk);
     if constexpr (RC == 1) {
-        if (E * lane_id() < valid)
-            __builtin_nontemporal_store(pk[0], reinterpret_cast<u32x4 *>(dst) + lane_id());
+        if (E * el < valid)
+            __builtin_nontemporal_store(pk[0], reinterpret_cast<u32x4 *>(dst) + el);
     } else {
-        stage_out<RC>(reinterpret_cast<u32x4 *>(dst), valid * BITS / 128, lds, pk);
+        stage_out<RC>(reinterpret_cast<u32x4 *>(dst), valid * BITS / 128, lds, pk, el);
     }
+}
+
+template <int E, int BITS>
+SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, const uint32_t (&q)[E])
+{
+    store_codes<E, BITS>(dst, valid, lds, q, lane_id());
 }
 
 template <int E, int NB>
@@ -187,6 +193,17 @@ SDP4_DEV void maybe_fwht(float (&v)[E], float cn)
 {
     if constexpr (NB > 1)
         fwht_lane<E, NB>(v, cn);
+}
+
+// Fused transform of a kernel whose lanes follow element_lane when blocks
+// span several lanes (NB > E); within one lane, the plain transform.
+template <int E, int NB>
+SDP4_DEV void fused_fwht(float (&v)[E], float cn, int el)
+{
+    if constexpr (NB > E)
+        fwht_lane_signed<E, NB>(v, cn, el);
+    else
+        maybe_fwht<E, NB>(v, cn);
 }
 
 // ---------------------------------------------------------------------------
@@ -438,6 +455,8 @@ __global__ __launch_bounds__(kWave * WPB) void k_grad_quant(
     __shared__ u32x4 lds_all[WPB][kWave * R];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
+    const int el = NB > E ? element_lane(lane) : lane; // element lane of this lane
+    const int off = E * el;
     const int gs = group_shift(group);
     const int lanes_per_group = group / E;
     struct Tile {
@@ -453,10 +472,10 @@ __global__ __launch_bounds__(kWave * WPB) void k_grad_quant(
         float v[E];
         {
             u32x4 c[R];
-            transpose_in<R>(in.a, lds, c);
+            transpose_in<R>(in.a, lds, c, el);
             chunks_to_f32<E>(c, v);
         }
-        maybe_fwht<E, NB>(v, cn);
+        fused_fwht<E, NB>(v, cn, el);
         float a = 0.0f;
 #pragma unroll
         for (int i = 0; i < E; ++i)
@@ -467,7 +486,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_grad_quant(
         uint32_t q[E];
         if constexpr (SR) {
             float u[E];
-            sr_uniforms<E>(seed, offset + (uint64_t)(base + E * lane), u);
+            sr_uniforms<E>(seed, offset + (uint64_t)(base + off), u);
 #pragma unroll
             for (int i = 0; i < E; ++i)
                 q[i] = code_bits_sr(v[i], inv, u[i], qmax);
@@ -476,8 +495,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_grad_quant(
             for (int i = 0; i < E; ++i)
                 q[i] = code_bits(v[i], inv);
         }
-        store_codes<E, BITS>(codes + base * BITS / 8, valid, lds, q);
-        const int off = E * lane;
+        store_codes<E, BITS>(codes + base * BITS / 8, valid, lds, q, el);
         if (off < valid && (off & (group - 1)) == 0)
             scale[(base + off) >> gs] = s;
     };
@@ -500,6 +518,9 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
     __shared__ u32x4 lds_all[WPB][kWave * R];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
+    // element lane: relabeled when the fused inverse transform spans lanes
+    const int el = (BITS_OUT == 0 && NB > E) ? element_lane(lane) : lane;
+    const int off = E * el;
     const int gs = group_shift(group);
     struct Tile {
         u32x4 c[PMAX][CW];
@@ -507,7 +528,6 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
     };
     auto load = [&](int64_t t, Tile &in) {
         const int64_t base = t * W;
-        const int off = E * lane;
         const bool active = off < tile_valid(n, base, W);
         const int64_t gi = (base + off) >> gs;
 #pragma unroll
@@ -539,7 +559,6 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
     auto proc = [&](int64_t t, Tile &in) {
         const int64_t base = t * W;
         const int valid = tile_valid(n, base, W);
-        const int off = E * lane;
         float acc[E];
 #pragma unroll
         for (int i = 0; i < E; ++i)
@@ -549,7 +568,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
             if (j < P) {
                 if constexpr (SDP4_PEER_LDS && CW > 1) {
                     u32x4 tmp[CW];
-                    transpose_in<CW>(in.c[j], lds, tmp);
+                    transpose_in<CW>(in.c[j], lds, tmp, el);
 #pragma unroll
                     for (int k = 0; k < CW; ++k)
                         in.c[j][k] = tmp[k];
@@ -568,7 +587,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
             }
         }
         if constexpr (BITS_OUT == 0) {
-            maybe_fwht<E, NB>(acc, cn);
+            fused_fwht<E, NB>(acc, cn, el);
             if (out_scale != 1.0f) {
 #pragma unroll
                 for (int i = 0; i < E; ++i)
@@ -576,7 +595,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
             }
             u32x4 c[R];
             f32_to_chunks<E>(acc, c);
-            stage_out<R>(reinterpret_cast<u32x4 *>(out_f32 + base), valid / 4, lds, c);
+            stage_out<R>(reinterpret_cast<u32x4 *>(out_f32 + base), valid / 4, lds, c, el);
         } else {
             if (out_f32) {
                 u32x4 c[R];

@@ -3,8 +3,8 @@ max(group, block), from one segment to dozens of wave tiles), bit widths,
 Hadamard blocks, groups, peer counts, offsets and value distributions
 (normal, heavy-tailed, one-signed, sparse, constant runs, mixed
 magnitudes spanning 1e-30..1e30, exact lattice points) and compares every
-entry point with the oracle.  Examples are derandomized so a run on the
-GPU machine is reproducible."""
+entry point with the oracle.  Examples are derandomized so every GPU run
+draws the same cases."""
 import numpy as np
 import pytest
 

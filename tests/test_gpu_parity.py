@@ -309,6 +309,37 @@ def test_dequant_reduce_wide_group_to_f32():
     check_f32(host(of), ref["f32"])
 
 
+@pytest.mark.parametrize("bits_in", [4, 8])
+@pytest.mark.parametrize("block", [64, 256, 512, 1024])
+@pytest.mark.parametrize("out_scale", [1.0, -0.5])
+def test_dequant_reduce_to_f32_exact_zeros(bits_in, block, out_scale):
+    """Exact zeros out of the inverse transform carry the oracle's sign bit.
+    Two peers send equal codes for elements 2j and 2j+1 (one group, power-of-two
+    scales, so every product is exact): every odd output of a block is then an
+    exact zero, and in every third group the second peer negates the first, so
+    whole groups reduce to zero."""
+    group = 128
+    n = size_for(max(group, block), 16384)
+    say(f"dequant_reduce f32 exact zeros in={bits_in} block={block} out_scale={out_scale} n={n}")
+    rng = np.random.default_rng(block + bits_in)
+    qmax = 127 if bits_in == 8 else 7
+    q0 = rng.integers(-qmax, qmax + 1, n // 2).repeat(2)
+    q1 = rng.integers(-qmax, qmax + 1, n // 2).repeat(2)
+    q1 = np.where((np.arange(n) // group) % 3 == 0, -q0, q1)
+    sc = (np.float32(2.0) ** rng.integers(-24, -4, n // group)).astype(np.float32)
+    if bits_in == 8:
+        codes = [q.astype(np.int8).view(np.uint8) for q in (q0, q1)]
+    else:
+        codes = [oracle.pack4(q.astype(np.int32)) for q in (q0, q1)]
+    of = empty(n, "f32")
+    sdp4.sdp4_dequant_reduce([dev(c) for c in codes], [dev(sc), dev(sc)], n, bits_in, group, 0, block,
+                             out_scale, None, None, of)
+    sync()
+    ref = oracle.dequant_reduce(codes, [sc, sc], n, bits_in, group, 0, block, out_scale)
+    assert np.count_nonzero(ref["f32"] == 0) >= n // 2
+    check_f32(host(of), ref["f32"])
+
+
 # ----------------------------------------------------------------------------
 # standalone pieces of the unfused variant
 # ----------------------------------------------------------------------------
