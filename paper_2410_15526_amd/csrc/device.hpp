@@ -248,25 +248,24 @@ SDP4_DEV void bf16_chunks_to_f32(const u32x4 (&c)[E / 8], float (&v)[E])
     }
 }
 
-// float -> bfloat16 bits, round to nearest even (finite inputs)
-SDP4_DEV uint32_t bf16_rne_bits(float f)
+// Two floats -> packed bfloat16 (first in the low half), round to nearest
+// even: one v_cvt_pk_bf16_f32 on gfx950 (finite inputs; denormals kept).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+SDP4_DEV uint32_t bf16x2_rne(float a, float b)
 {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return u >> 16;
+    const f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 template <int E>
 SDP4_DEV void f32_to_bf16_chunks(const float (&v)[E], u32x4 (&c)[E / 8])
 {
 #pragma unroll
-    for (int k = 0; k < E / 8; ++k) {
-        uint32_t w[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            w[j] = bf16_rne_bits(v[8 * k + 2 * j]) | (bf16_rne_bits(v[8 * k + 2 * j + 1]) << 16);
-        c[k] = u32x4{w[0], w[1], w[2], w[3]};
-    }
+    for (int k = 0; k < E / 8; ++k)
+        c[k] = u32x4{bf16x2_rne(v[8 * k], v[8 * k + 1]), bf16x2_rne(v[8 * k + 2], v[8 * k + 3]),
+                     bf16x2_rne(v[8 * k + 4], v[8 * k + 5]), bf16x2_rne(v[8 * k + 6], v[8 * k + 7])};
 }
 
 // ---------------------------------------------------------------------------

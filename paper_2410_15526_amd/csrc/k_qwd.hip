@@ -32,10 +32,10 @@ template <int E>
 int qwd_decode_e(const uint8_t *codes, const float *scale, const float *minv, int64_t n, int group,
                  void *w_prev, bool bf16, bool sym, hipStream_t s)
 {
-    constexpr int WPB = kWavesPerBlock;
+    constexpr int WPB = kDecWaves;
     auto k = bf16 ? (sym ? k_qwd_decode<true, true, E, kDepth, WPB> : k_qwd_decode<true, false, E, kDepth, WPB>)
                   : (sym ? k_qwd_decode<false, true, E, kDepth, WPB> : k_qwd_decode<false, false, E, kDepth, WPB>);
-    return launch<WPB>(k, wave_blocks<WPB>(n, E), kCap, s, codes, scale, minv, n, group, w_prev);
+    return launch<WPB>(k, wave_blocks<WPB>(n, E), kDecCap, s, codes, scale, minv, n, group, w_prev);
 }
 
 } // namespace

@@ -65,6 +65,27 @@
 #define SDP4_K1_BPC 1
 #endif
 
+// Block shapes of the qWD decoder, of the dequantize-reduce with
+// re-quantization (K2) and of the dequantize-reduce to float32 (K3).
+#ifndef SDP4_DEC_WAVES
+#define SDP4_DEC_WAVES 4
+#endif
+#ifndef SDP4_DEC_BPC
+#define SDP4_DEC_BPC 1
+#endif
+#ifndef SDP4_RQ_WAVES
+#define SDP4_RQ_WAVES 4
+#endif
+#ifndef SDP4_RQ_BPC
+#define SDP4_RQ_BPC 2
+#endif
+#ifndef SDP4_RF_WAVES
+#define SDP4_RF_WAVES 4
+#endif
+#ifndef SDP4_RF_BPC
+#define SDP4_RF_BPC 2
+#endif
+
 #ifndef SDP4_ENC_PHASE_US
 #define SDP4_ENC_PHASE_US 44 // qWD encoder read/write period in microseconds (0: ordinary stream)
 #endif
@@ -419,15 +440,24 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_decode(
         else
             chunks_to_f32<E>(c, w);
 #pragma unroll
-        for (int i = 0; i < E; ++i) {
-            const uint32_t word = in.c[i / 32][(i / 8) % 4];
+        for (int k = 0; k < E / 8; ++k) { // word k: the nibbles of elements 8k .. 8k+7, even ones low
+            const uint32_t word = in.c[k / 4][k % 4];
             if constexpr (SYM) {
-                const float code = (float)((int32_t)(word << (28 - 4 * (i % 8))) >> 28);
-                const float value = code * in.s;
-                w[i] = w[i] + value;
+#pragma unroll
+                for (int m = 0; m < 8; ++m) {
+                    const float code = (float)((int32_t)(word << (28 - 4 * m)) >> 28);
+                    const float value = code * in.s;
+                    w[8 * k + m] = w[8 * k + m] + value;
+                }
             } else {
-                const float code = (float)((word >> (4 * (i % 8))) & 0xFu);
-                w[i] = w[i] + __builtin_fmaf(code, in.s, in.mn);
+                // byte j of lo / hi: the code of element 8k + 2j / 8k + 2j + 1
+                const uint32_t lo = word & 0x0F0F0F0Fu, hi = (word >> 4) & 0x0F0F0F0Fu;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float c0 = (float)((lo >> (8 * j)) & 0xFFu), c1 = (float)((hi >> (8 * j)) & 0xFFu);
+                    w[8 * k + 2 * j] = w[8 * k + 2 * j] + __builtin_fmaf(c0, in.s, in.mn);
+                    w[8 * k + 2 * j + 1] = w[8 * k + 2 * j + 1] + __builtin_fmaf(c1, in.s, in.mn);
+                }
             }
         }
         if constexpr (BF16) {
@@ -676,6 +706,8 @@ int64_t wave_blocks(int64_t n, int E)
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
 constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC;
 constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
+constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
+constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
 
 // 64 elements per lane: required for groups of 4096 (a group must fit one
 // wavefront), allowed (preferred_e == 64) for any group of at least 64 (a
@@ -713,14 +745,15 @@ int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, flo
               uint64_t offset = 0)
 {
     constexpr int pipe = BITS_OUT == 0 ? kDepth : 0;
-    constexpr int WPB = kWavesPerBlock;
+    constexpr int WPB = BITS_OUT == 0 ? kRfWaves : kRqWaves;
+    constexpr int cap = BITS_OUT == 0 ? kRfCap : kRqCap;
     if (P <= 4)
-        return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe, WPB, SR>, wave_blocks<WPB>(n, E), kCap,
+        return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe, WPB, SR>, wave_blocks<WPB>(n, E), cap,
                            s, peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
     if (P <= 8)
-        return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe, WPB, SR>, wave_blocks<WPB>(n, E), kCap,
+        return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 8, pipe, WPB, SR>, wave_blocks<WPB>(n, E), cap,
                            s, peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
-    return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, 0, WPB, SR>, wave_blocks<WPB>(n, E), kCap, s,
+    return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 16, 0, WPB, SR>, wave_blocks<WPB>(n, E), cap, s,
                        peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
 }
 

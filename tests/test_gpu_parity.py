@@ -171,6 +171,50 @@ def test_qwd_edge_values(prev_dtype):
         check_f32(upd, want)
 
 
+def test_qwd_decode_bf16_rounding_edges():
+    """bf16 model weights: the fp32 sum is narrowed with round-to-nearest-even
+    at exact ties (both parities, both signs), on denormals and at the top of
+    the range (a tie above the largest bf16 goes to infinity).  Scales are 0,
+    so each group adds its minimum to every weight."""
+    g, ng = 128, 24
+    n = g * ng
+    rng = np.random.default_rng(5)
+    prev_f = np.empty(n, np.float32)
+    mn = np.zeros(ng, np.float32)
+    ones_to_two = 1.0 + rng.integers(0, 128, n).astype(np.float32) / 128   # bf16-exact values in [1, 2)
+    for k in range(ng):
+        sl = slice(k * g, (k + 1) * g)
+        kind = k % 8
+        if kind == 0:                       # ties at half a bf16 step in [1, 2)
+            prev_f[sl], mn[k] = ones_to_two[sl], 2.0 ** -8
+        elif kind == 1:                     # negative ties
+            prev_f[sl], mn[k] = -ones_to_two[sl], -(2.0 ** -8)
+        elif kind == 2:                     # 3/2 of a step: ties above the next value
+            prev_f[sl], mn[k] = ones_to_two[sl], 3 * 2.0 ** -8
+        elif kind == 3:                     # zero weights plus an fp32 denormal
+            prev_f[sl], mn[k] = 0.0, np.float32(1e-40) * (k + 1)
+        elif kind == 4:                     # bf16 denormal weights plus a denormal
+            prev_f[sl] = (rng.integers(-127, 128, g) * 2.0 ** -133).astype(np.float32)
+            mn[k] = np.float32(2.0 ** -134 + 2.0 ** -140)
+        elif kind == 5:                     # largest bf16 plus half its step: a tie that overflows
+            prev_f[sl], mn[k] = np.float32(3.3895313892515355e38), np.float32(2.0 ** 119)
+        elif kind == 6:                     # one fp32 step below that tie: stays finite
+            prev_f[sl], mn[k] = np.float32(3.3895313892515355e38), np.float32(2.0 ** 119 - 2.0 ** 104)
+        else:                               # ordinary values
+            prev_f[sl], mn[k] = (rng.standard_normal(g) * 0.02).astype(np.float32), np.float32(1.7e-3)
+    prev = oracle.bf16_rne(prev_f)
+    codes = np.zeros(n // 2, np.uint8)
+    scale = np.zeros(ng, np.float32)
+    say("qwd decode bf16 rounding edges")
+    pd = dev(prev)
+    sdp4.sdp4_qwd_decode(dev(codes), dev(scale), dev(mn), g, pd)
+    sync()
+    want = oracle.qwd_decode(codes, scale, mn, prev, g)
+    got = host(pd)
+    assert np.array_equal(got, want), np.nonzero(got != want)[0][:10]
+    assert np.all(want[5 * g:6 * g] == 0x7F80) and np.all(want[6 * g:7 * g] == 0x7F7F)
+
+
 def test_qw_variant_is_encode_from_zero():
     """qW (direct 4-bit weight quantization, Sec. 5.1 baseline) = qWD against zero weights."""
     n, g = size_for(2048), 2048
