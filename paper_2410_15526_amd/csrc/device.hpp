@@ -374,12 +374,14 @@ SDP4_DEV void fwht_cross_signed(float (&v)[E], int el)
     }
 }
 
-// The butterfly stages of fwht_lane on relabeled lanes (element lane el):
+// The blockwise transform of fwht_lane on relabeled lanes (element lane el):
 // the same stages in the same order with the same roundings, cross-lane
-// stages as fwht_cross_signed, no final scaling.  Returns the sign the
-// lane's values then carry, (-1)^popcount(el & (NB/E - 1)).
+// stages as fwht_cross_signed.  After the last stage a lane's values carry
+// the sign (-1)^popcount(el & (NB/E - 1)), which the final scaling by +-cn
+// removes; it is one fma with a +0 addend, so an exact zero comes out as +0
+// (the only difference from fwht_lane: -0 results become +0).
 template <int E, int NB>
-SDP4_DEV float fwht_lane_signed_unscaled(float (&v)[E], int el)
+SDP4_DEV void fwht_lane_signed(float (&v)[E], float cn, int el)
 {
     static_assert(NB > E && (NB & (NB - 1)) == 0 && NB <= 64 * E, "block");
 #pragma unroll
@@ -399,16 +401,7 @@ SDP4_DEV float fwht_lane_signed_unscaled(float (&v)[E], int el)
     if constexpr (NB > 8 * E) fwht_cross_signed<E, 8>(v, el);
     if constexpr (NB > 16 * E) fwht_cross_signed<E, 16>(v, el);
     if constexpr (NB > 32 * E) fwht_cross_signed<E, 32>(v, el);
-    return (__builtin_popcount(el & (NB / E - 1)) & 1) ? -1.0f : 1.0f;
-}
-
-// The whole transform on relabeled lanes: the stages, then the scaling by
-// cn times the lane's sign as one fma with a +0 addend, so an exact zero
-// comes out as +0 (the only difference from fwht_lane: -0 results become +0).
-template <int E, int NB>
-SDP4_DEV void fwht_lane_signed(float (&v)[E], float cn, int el)
-{
-    const float c = fwht_lane_signed_unscaled<E, NB>(v, el) * cn;
+    const float c = (__builtin_popcount(el & (NB / E - 1)) & 1) ? -cn : cn;
 #pragma unroll
     for (int i = 0; i < E; ++i)
         v[i] = __builtin_fmaf(v[i], c, 0.0f);
