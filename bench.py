@@ -14,7 +14,7 @@ kernel the line also carries algorithmic HBM bytes / launch time against the
 largest share of the step.  ``cpu_baseline`` is the plain CPU oracle timed
 on a bounded sample of the same workload on this host (single thread).
 
-Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload c5]
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 20] [--workload c5]
 """
 from __future__ import annotations
 
@@ -83,6 +83,20 @@ def traffic_for(kernel: str, workload: str = "c5"):
     return None if k is None else k.get("bytes_per_launch")
 
 
+def host_cpu() -> str:
+    """Model name of this host's CPU and the cores this process may use."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{name}, {len(os.sched_getaffinity(0))} cores available"
+
+
 def cpu_baseline(w, sample_log2: int, seed: int):
     """The oracle on a contiguous sample of the workload: one full step."""
     import numpy as np
@@ -106,7 +120,7 @@ def cpu_baseline(w, sample_log2: int, seed: int):
     dt = time.perf_counter() - t0
     fp32_bytes = 4 * (n + n + n + n + n // P)
     return {"value": round(fp32_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "seconds": round(dt, 3),
+            "seconds": round(dt, 3), "host_cpu": host_cpu(),
             "sample": f"elements [0, 2^{sample_log2}) of the same workload, one full step "
                       f"(qWD encode+decode, Hadamard+8-bit, 8-bit x{P} reduce + 4-bit, 4-bit x{Q} reduce + "
                       f"inverse Hadamard), single-threaded plain C oracle"}
@@ -116,7 +130,7 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="c5")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-sample-log2", type=int, default=29)
@@ -179,10 +193,14 @@ def main():
     info = hp.kernel_info()
     kernels = {}
     for name, pairs in events.items():
-        ms = sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
+        per = sorted(a.elapsed_time(b) for a, b in pairs)
+        ms = sum(per) / len(per)
+        med = per[len(per) // 2] if len(per) % 2 else 0.5 * (per[len(per) // 2 - 1] + per[len(per) // 2])
+        std = (sum((x - ms) ** 2 for x in per) / max(len(per) - 1, 1)) ** 0.5
         ki = info[name]
         alg = ki.alg_bytes / (ms * 1e-3) / 1e9
-        kernels[name] = {"ms": round(ms, 4), "alg_bytes": ki.alg_bytes, "alg_GBps": round(alg, 1),
+        kernels[name] = {"ms": round(ms, 4), "ms_median": round(med, 4), "ms_std": round(std, 4),
+                         "alg_bytes": ki.alg_bytes, "alg_GBps": round(alg, 1),
                          "hbm_frac": round(alg / HBM_PEAK_GBPS, 4),
                          "fp32_in_GBps": round(ki.fp32_in_bytes / (ms * 1e-3) / 1e9, 1),
                          "elems_per_s": round(ki.fp32_in_bytes / 4 / (ms * 1e-3), 1)}
