@@ -2,7 +2,9 @@
 of a clock period, outputs buffered in LDS and written in the rest) against
 the oracle on every element: groups 128..1024, both codecs, float32 and
 bfloat16 model weights, and a shard whose last wave tile is partial.  The
-8-bit K1 is checked at the same size (it streams without phases)."""
+8-bit K1 and the 4-bit re-quantizing dequantize-reduce (K2: 8- and 4-bit peer
+messages, 2..16 peers) are checked at the same size; they stream without
+phases."""
 import numpy as np
 import pytest
 
@@ -65,3 +67,23 @@ def test_large_k1_matches_oracle(block, group):
     rc, rs, pre = oracle.grad_quant(x, 8, block, group)
     check_headers(host(scale), rs)
     check_codes(host(codes), rc, pre, N, 8)
+
+
+@pytest.mark.parametrize("P,bits_in,group", [(8, 8, 128), (3, 8, 256), (2, 8, 1024), (4, 4, 128), (16, 4, 512)])
+def test_large_requant_matches_oracle(P, bits_in, group):
+    """Dequantize-reduce over P peers with 4-bit re-quantization (K2), every element."""
+    say(f"large dequant_reduce requant P={P} in={bits_in} group={group} n={N}")
+    r = np.random.default_rng(100 * P + bits_in + group)
+    qmax = 127 if bits_in == 8 else 7
+    codes, scales = [], []
+    for _ in range(P):
+        q = r.integers(-qmax, qmax + 1, N).astype(np.int8)
+        codes.append(q.view(np.uint8) if bits_in == 8 else oracle.pack4(q))
+        scales.append((r.random(N // group) * 1e-4).astype(np.float32))
+    oc, osc = empty(N // 2, "u8"), empty(N // group, "f32")
+    sdp4.sdp4_dequant_reduce([dev(c) for c in codes], [dev(x) for x in scales], N, bits_in, group, 4, 0, 1.0,
+                             oc, osc, None)
+    torch().cuda.synchronize()
+    ref = oracle.dequant_reduce(codes, scales, N, bits_in, group, 4)
+    check_headers(host(osc), ref["scales"])
+    check_codes(host(oc), ref["codes"], ref["pre"], N, 4)
