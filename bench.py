@@ -162,7 +162,20 @@ def main():
     torch.cuda.synchronize()
     log(f"inputs ready in {time.perf_counter() - t_fill:.1f} s: {w.describe()}")
 
-    # copy-kernel yardstick (2 GiB read + 2 GiB written)
+    for _ in range(args.warmup):
+        hp.step()
+    torch.cuda.synchronize()
+    events = {}
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        hp.step(events=events)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
+
+    # copy-kernel yardstick (2 GiB read + 2 GiB written), after the timed steps so that it runs on a
+    # GPU as warm as the one the steps ran on
     cn = 1 << 29
     src = torch.empty(cn, device="cuda")
     dst = torch.empty(cn, device="cuda")
@@ -177,18 +190,6 @@ def main():
     torch.cuda.synchronize()
     copy_gbps = 2 * 4 * cn * 10 / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
     del src, dst
-
-    for _ in range(args.warmup):
-        hp.step()
-    torch.cuda.synchronize()
-    events = {}
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        hp.step(events=events)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / args.steps
-    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
 
     info = hp.kernel_info()
     kernels = {}

@@ -87,16 +87,23 @@
 #endif
 
 #ifndef SDP4_ENC_PHASE_US
-#define SDP4_ENC_PHASE_US 44 // qWD encoder read/write period in microseconds (0: ordinary stream)
+#define SDP4_ENC_PHASE_US 50 // qWD encoder read/write period in microseconds (0: ordinary stream)
 #endif
 #ifndef SDP4_ENC_READ_PCT
 #define SDP4_ENC_READ_PCT 90 // per cent of the period spent reading
+#endif
+#ifndef SDP4_ENC_PHASE_DEPTH
+#define SDP4_ENC_PHASE_DEPTH 1 // tiles each phased encoder wave keeps loading ahead
+#endif
+#ifndef SDP4_ENC_PHASE_CAP
+#define SDP4_ENC_PHASE_CAP 27 // tiles of codes and headers each encoder wave buffers in LDS
 #endif
 
 namespace sdp4 {
 
 constexpr int kDepth = SDP4_PIPE;
-constexpr int kEncPhaseCap = 24;            // tiles buffered per wave by the phased encoder
+constexpr int kEncPhaseCap = SDP4_ENC_PHASE_CAP; // tiles buffered per wave by the phased encoder
+constexpr int kEncPhaseDepth = SDP4_ENC_PHASE_DEPTH;
 constexpr int kEncPhaseMinGroup = 128;      // smallest group the phased encoder buffers headers for
 constexpr int64_t kPhaseMinElements = 1 << 26; // smaller launches use the ordinary stream
 
@@ -146,38 +153,48 @@ SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base 
 // wave-private LDS buffer of up to `cap` tiles, which they write out in the
 // rest of the period -- so the memory system sees long read-only and
 // write-only stretches instead of a mix.  proc(t, in, slot) computes tile t
-// into buffer slot `slot`; flush(k) writes slots 0..k-1.  One tile is
-// prefetched.  Every wait is a short sleep until the clock moves to the
+// into buffer slot `slot`; flush(k) writes slots 0..k-1.  DEPTH tiles are
+// prefetched (a ring of register buffers, indexed at compile time by
+// unrolling).  Every wait is a short sleep until the clock moves to the
 // other phase, and the loop ends once the wave has no tile left and an
 // empty buffer, so every wave exits.  Results do not depend on the timing.
-template <int WPB, class Tile, class Load, class Proc, class Flush>
+template <int DEPTH, int WPB, class Tile, class Load, class Proc, class Flush>
 SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_t read_ticks, Load load, Proc proc,
                                Flush flush)
 {
+    static_assert(DEPTH >= 1, "depth");
     const int wave = threadIdx.x / kWave;
     const int64_t stride = (int64_t)gridDim.x * WPB;
     int64_t t = (int64_t)blockIdx.x * WPB + wave;
-    Tile in;
-    bool have = t < ntiles;
-    if (have)
-        load(t, in);
+    Tile buf[DEPTH];
+#pragma unroll
+    for (int k = 0; k < DEPTH; ++k)
+        if (t + k * stride < ntiles)
+            load(t + k * stride, buf[k]);
     int nbuf = 0;
     for (;;) {
-        const bool reading = (uint64_t)wall_clock64() % period < read_ticks;
-        if (have && nbuf < cap && reading) {
-            proc(t, in, nbuf);
-            ++nbuf;
-            t += stride;
-            have = t < ntiles;
-            if (have)
-                load(t, in);
-        } else if (nbuf > 0 && (!reading || !have)) {
-            flush(nbuf);
-            nbuf = 0;
-        } else if (!have) {
-            break; // no tile left and the buffer is empty
-        } else {
-            __builtin_amdgcn_s_sleep(1); // buffer full in a read phase, or empty in a write phase
+#pragma unroll
+        for (int k = 0; k < DEPTH; ++k) {
+            // tile t is in buf[k]; wait until it may be processed
+            for (;;) {
+                const bool have = t < ntiles;
+                const bool reading = (uint64_t)wall_clock64() % period < read_ticks;
+                if (have && nbuf < cap && reading) {
+                    proc(t, buf[k], nbuf);
+                    ++nbuf;
+                    if (t + DEPTH * stride < ntiles)
+                        load(t + DEPTH * stride, buf[k]);
+                    t += stride;
+                    break;
+                } else if (nbuf > 0 && (!reading || !have)) {
+                    flush(nbuf);
+                    nbuf = 0;
+                } else if (!have) {
+                    return; // no tile left and the buffer is empty
+                } else {
+                    __builtin_amdgcn_s_sleep(1); // buffer full in a read phase, or empty in a write phase
+                }
+            }
         }
     }
 }
@@ -378,7 +395,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
             }
             wave_lds_sync();
         };
-        phased_tile_loop<WPB, Tile>(ntiles, CAP, period, read_ticks, load, proc, flush);
+        phased_tile_loop<kEncPhaseDepth, WPB, Tile>(ntiles, CAP, period, read_ticks, load, proc, flush);
     }
 }
 
