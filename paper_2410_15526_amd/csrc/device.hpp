@@ -2,10 +2,13 @@
 //
 // Register layout used by every element-wise kernel: a wavefront owns a
 // "wave tile" of 64*E consecutive elements and lane l holds the E
-// consecutive elements [E*l, E*l + E) of it.  Quantization groups and
+// consecutive elements [E*el, E*el + E) of it, where the element lane el is
+// l itself, or, in the kernels whose Hadamard blocks span several lanes, a
+// fixed permutation of l inside each row of 16 lanes (element_lane) that
+// puts every butterfly partner within DPP reach.  Quantization groups and
 // Hadamard blocks are aligned to E-element lane slices (group >= E), so a
 // group or block is either inside one lane (handled in registers) or spans
-// 2^k neighbouring lanes (handled with cross-lane exchanges).
+// an aligned block of 2^k lanes (handled with cross-lane exchanges).
 //
 // Global memory is read and written in the coalesced order (instruction i,
 // lane l touches the 16-byte chunk 64*i + l of the tile) and transposed to
@@ -275,7 +278,9 @@ SDP4_DEV void f32_to_bf16_chunks(const float (&v)[E], u32x4 (&c)[E / 8])
 // multiplication by cn.  Widths below E pair registers of one lane; width
 // h >= E pairs register i of lane l with register i of lane l ^ (h / E):
 // the lower lane keeps a + b and the upper one a - b, both computed as a
-// single-rounding fma(own, +-1, other).
+// single-rounding fma(own, +-1, other).  This form keeps the sign of every
+// zero as the plain butterfly does; the standalone transform uses it.  The
+// fused kernels use the cheaper relabeled form further below.
 template <int E, int D>
 SDP4_DEV void fwht_cross(float (&v)[E])
 {
