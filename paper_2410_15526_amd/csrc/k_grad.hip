@@ -17,6 +17,12 @@ struct GradQuant {
             return launch<WPB>(k, wave_blocks<WPB>(n, 64), kCap, s, x, n, group, cn, codes, scale, uint64_t(0),
                                uint64_t(0));
         }
+        if constexpr (NB == 0) {   // no transform: 32 elements per lane, its own block shape
+            constexpr int WPB = kK1PlainWaves;
+            auto k = bits == 8 ? k_grad_quant<8, 32, 0, kDepth, WPB> : k_grad_quant<4, 32, 0, kDepth, WPB>;
+            return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, uint64_t(0),
+                               uint64_t(0));
+        }
         if (bits == 8 && SDP4_E_K1 == 16 && group <= kWave * 16) {   // a group must fit one wavefront
             constexpr int WPB = kK1Waves;
             return launch<WPB>(k_grad_quant<8, 16, NB, kDepth, WPB>, wave_blocks<WPB>(n, 16), kK1Cap, s, x, n, group, cn,

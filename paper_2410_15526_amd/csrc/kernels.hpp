@@ -12,12 +12,13 @@
 //
 // The SDP4_* macros below are build-time tuning knobs; their defaults are
 // the measured best on MI355X: one tile prefetched, 32 elements per lane
-// (16 for the 8-bit K1), int8 peer chunks transposed through LDS, and per
-// kernel family a block shape -- one resident block of four waves per CU
-// for the qWD encoder, one block of eight waves for K1, two blocks of four
-// waves for the rest.  (How many bytes a CU keeps in flight, and how far
-// compute spreads its requests out, moves the mixed read/write bandwidth of
-// HBM by several per cent.)
+// (16 for the 8-bit K1 with a transform), int8 peer chunks transposed
+// through LDS, and per kernel family a block shape -- one resident block of
+// four waves per CU for the qWD encoder and decoder, one block of eight
+// waves for K1 (four without a transform), two blocks of four waves for the
+// rest.  (How many bytes a CU keeps in flight, and how far compute spreads
+// its requests out, moves the mixed read/write bandwidth of HBM by several
+// per cent.)
 #pragma once
 
 #include "device.hpp"
@@ -60,6 +61,9 @@
 #endif
 #ifndef SDP4_K1_WAVES_32
 #define SDP4_K1_WAVES_32 8 // K1 with 32 elements per lane (4-bit codes, stochastic rounding)
+#endif
+#ifndef SDP4_K1_WAVES_PLAIN
+#define SDP4_K1_WAVES_PLAIN 4 // K1 without a transform (32 elements per lane)
 #endif
 #ifndef SDP4_K1_BPC
 #define SDP4_K1_BPC 1
@@ -723,6 +727,7 @@ int64_t wave_blocks(int64_t n, int E)
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
 constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC;
 constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
+constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
 
