@@ -67,6 +67,11 @@ int launch_dequant_reduce(const PeerTable &peers, int P, int64_t n, int bits_in,
                    ? launch_dequant_reduce_f32_in8(peers, P, n, group, nblk, cn, out_scale, out_f32, s)
                    : launch_dequant_reduce_f32_in4(peers, P, n, group, nblk, cn, out_scale, out_f32, s);
     const bool wide = use_wide_lanes(group, SDP4_E_RED);
+    if (bits_in == 8 && SDP4_E_RQ8 == 16 && group <= kWave * 16) { // a group must fit one wavefront
+        if (bits_out == 4)
+            return dr_launch<8, 4, 16, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s);
+        return dr_launch<8, 8, 16, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s);
+    }
     if (bits_in == 8) {
         if (bits_out == 4)
             return wide ? dr_launch<8, 4, 64, 0>(peers, P, n, group, cn, 1.0f, out_codes, out_scales, out_f32, s)

@@ -12,11 +12,12 @@
 //
 // The SDP4_* macros below are build-time tuning knobs; their defaults are
 // the measured best on MI355X: one tile prefetched, 32 elements per lane
-// (16 for the 8-bit K1 with a transform), int8 peer chunks transposed
-// through LDS, and per kernel family a block shape -- one resident block of
-// four waves per CU for the qWD encoder and decoder, one block of eight
-// waves for K1 (four without a transform), two blocks of four waves for the
-// rest.  (How many bytes a CU keeps in flight, and how far compute spreads
+// (16 for the 8-bit K1 with a transform and for the re-quantizing
+// dequantize-reduce of 8-bit messages, so that each lane loads one 16-byte
+// chunk per peer), and per kernel family a block shape -- one resident
+// block of four waves per CU for the qWD encoder and decoder, one block of
+// eight waves for K1 (four without a transform) and for the 8-bit K2, two
+// blocks of four waves for the rest.  (How many bytes a CU keeps in flight, and how far compute spreads
 // its requests out, moves the mixed read/write bandwidth of HBM by several
 // per cent.)
 #pragma once
@@ -44,6 +45,9 @@
 #ifndef SDP4_E_RED
 #define SDP4_E_RED 32
 #endif
+#ifndef SDP4_E_RQ8
+#define SDP4_E_RQ8 16 // re-quantizing dequantize-reduce of 8-bit messages: one 16-byte chunk per peer and lane
+#endif
 #ifndef SDP4_BLOCKS_PER_CU
 #define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
 #endif
@@ -70,7 +74,8 @@
 #endif
 
 // Block shapes of the qWD decoder, of the dequantize-reduce with
-// re-quantization (K2) and of the dequantize-reduce to float32 (K3).
+// re-quantization (K2; 8-bit messages with 16 elements per lane have their
+// own) and of the dequantize-reduce to float32 (K3).
 #ifndef SDP4_DEC_WAVES
 #define SDP4_DEC_WAVES 4
 #endif
@@ -82,6 +87,12 @@
 #endif
 #ifndef SDP4_RQ_BPC
 #define SDP4_RQ_BPC 2
+#endif
+#ifndef SDP4_RQ8_WAVES // ... of 8-bit messages with 16 elements per lane
+#define SDP4_RQ8_WAVES 8
+#endif
+#ifndef SDP4_RQ8_BPC
+#define SDP4_RQ8_BPC 1
 #endif
 #ifndef SDP4_RF_WAVES
 #define SDP4_RF_WAVES 4
@@ -210,17 +221,24 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
 template <int E, int BITS>
 SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, const uint32_t (&q)[E], int el)
 {
-    constexpr int RC = E * BITS / 128; // 16-byte chunks per lane
-    u32x4 pk[RC];
-    if constexpr (BITS == 8)
-        pack8<E>(q, pk);
-    else
-        pack4<E>(q, pk);
-    if constexpr (RC == 1) {
+    if constexpr (E * BITS == 64) { // 16 nibbles: 8 bytes per lane, 512 contiguous bytes per wave
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
         if (E * el < valid)
-            __builtin_nontemporal_store(pk[0], reinterpret_cast<u32x4 *>(dst) + el);
+            __builtin_nontemporal_store(u32x2{pack_nibbles8(q), pack_nibbles8(q + 8)},
+                                        reinterpret_cast<u32x2 *>(dst) + el);
     } else {
-        stage_out<RC>(reinterpret_cast<u32x4 *>(dst), valid * BITS / 128, lds, pk, el);
+        constexpr int RC = E * BITS / 128; // 16-byte chunks per lane
+        u32x4 pk[RC];
+        if constexpr (BITS == 8)
+            pack8<E>(q, pk);
+        else
+            pack4<E>(q, pk);
+        if constexpr (RC == 1) {
+            if (E * el < valid)
+                __builtin_nontemporal_store(pk[0], reinterpret_cast<u32x4 *>(dst) + el);
+        } else {
+            stage_out<RC>(reinterpret_cast<u32x4 *>(dst), valid * BITS / 128, lds, pk, el);
+        }
     }
 }
 
@@ -730,6 +748,7 @@ constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = 
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
+constexpr int kRq8Waves = SDP4_RQ8_WAVES, kRq8Cap = SDP4_RQ8_BPC;
 
 // 64 elements per lane: required for groups of 4096 (a group must fit one
 // wavefront), allowed (preferred_e == 64) for any group of at least 64 (a
@@ -767,8 +786,8 @@ int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, flo
               uint64_t offset = 0)
 {
     constexpr int pipe = BITS_OUT == 0 ? kDepth : 0;
-    constexpr int WPB = BITS_OUT == 0 ? kRfWaves : kRqWaves;
-    constexpr int cap = BITS_OUT == 0 ? kRfCap : kRqCap;
+    constexpr int WPB = BITS_OUT == 0 ? kRfWaves : E == 16 ? kRq8Waves : kRqWaves;
+    constexpr int cap = BITS_OUT == 0 ? kRfCap : E == 16 ? kRq8Cap : kRqCap;
     if (P <= 4)
         return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe, WPB, SR>, wave_blocks<WPB>(n, E), cap,
                            s, peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
