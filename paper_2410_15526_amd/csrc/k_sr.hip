@@ -35,6 +35,13 @@ int launch_dequant_reduce_sr(const PeerTable &peers, int P, int64_t n, int bits_
                              float *out_f32, hipStream_t s)
 {
     const bool wide = use_wide_lanes(group, SDP4_E_RED);
+    if (bits_in == 8 && SDP4_E_RQ8 == 16 && group <= kWave * 16) { // a group must fit one wavefront
+        if (bits_out == 4)
+            return dr_launch<8, 4, 16, 0, true>(peers, P, n, group, 1.0f, 1.0f, out_codes, out_scales, out_f32, s, seed,
+                                                offset);
+        return dr_launch<8, 8, 16, 0, true>(peers, P, n, group, 1.0f, 1.0f, out_codes, out_scales, out_f32, s, seed,
+                                            offset);
+    }
     if (bits_in == 8) {
         if (bits_out == 4)
             return wide ? dr_launch<8, 4, 64, 0, true>(peers, P, n, group, 1.0f, 1.0f, out_codes, out_scales, out_f32,

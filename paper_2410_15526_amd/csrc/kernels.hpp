@@ -46,7 +46,7 @@
 #define SDP4_E_RED 32
 #endif
 #ifndef SDP4_E_RQ8
-#define SDP4_E_RQ8 16 // re-quantizing dequantize-reduce of 8-bit messages: one 16-byte chunk per peer and lane
+#define SDP4_E_RQ8 16 // re-quantizing dequantize-reduce of 8-bit messages (also stochastically rounded): one 16-byte chunk per peer and lane
 #endif
 #ifndef SDP4_BLOCKS_PER_CU
 #define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
