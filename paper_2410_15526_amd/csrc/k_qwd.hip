@@ -21,8 +21,12 @@ int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, in
         const int khz = wall_clock_khz(err);
         if (err != hipSuccess)
             return set_hip_error(err);
-        period = (uint64_t)khz * SDP4_ENC_PHASE_US / 1000;
+        period = khz > 0 ? (uint64_t)khz * SDP4_ENC_PHASE_US / 1000 : 0;
         read_ticks = period * SDP4_ENC_READ_PCT / 100;
+        // Both phases must last at least one clock tick, or a wave could wait
+        // for a phase that never comes: otherwise stream.
+        if (read_ticks == 0 || read_ticks >= period)
+            period = read_ticks = 0;
     }
     return launch<WPB>(k, wave_blocks<WPB>(n, E), kEncCap, s, w_new, w_prev, n, group, codes, scale, minv, period,
                        read_ticks);

@@ -119,6 +119,8 @@ namespace sdp4 {
 constexpr int kDepth = SDP4_PIPE;
 constexpr int kEncPhaseCap = SDP4_ENC_PHASE_CAP; // tiles buffered per wave by the phased encoder
 constexpr int kEncPhaseDepth = SDP4_ENC_PHASE_DEPTH;
+static_assert(SDP4_ENC_READ_PCT > 0 && SDP4_ENC_READ_PCT < 100, "the encoder's read phase is part of its period");
+static_assert(SDP4_ENC_PHASE_CAP >= 1 && SDP4_ENC_PHASE_DEPTH >= 1, "phased encoder buffers");
 constexpr int kEncPhaseMinGroup = 128;      // smallest group the phased encoder buffers headers for
 constexpr int64_t kPhaseMinElements = 1 << 26; // smaller launches use the ordinary stream
 
@@ -171,8 +173,9 @@ SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base 
 // into buffer slot `slot`; flush(k) writes slots 0..k-1.  DEPTH tiles are
 // prefetched (a ring of register buffers, indexed at compile time by
 // unrolling).  Every wait is a short sleep until the clock moves to the
-// other phase, and the loop ends once the wave has no tile left and an
-// empty buffer, so every wave exits.  Results do not depend on the timing.
+// other phase (0 < read_ticks < period, so both phases come round), and the
+// loop ends once the wave has no tile left and an empty buffer, so every
+// wave exits.  Results do not depend on the timing.
 template <int DEPTH, int WPB, class Tile, class Load, class Proc, class Flush>
 SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_t read_ticks, Load load, Proc proc,
                                Flush flush)
