@@ -190,13 +190,20 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
         if (t + k * stride < ntiles)
             load(t + k * stride, buf[k]);
     int nbuf = 0;
+    // Phase boundaries on the common grid of multiples of `period`, found by
+    // one division here and then advanced by additions.
+    uint64_t now = (uint64_t)wall_clock64();
+    uint64_t start = now - now % period;
     for (;;) {
 #pragma unroll
         for (int k = 0; k < DEPTH; ++k) {
             // tile t is in buf[k]; wait until it may be processed
             for (;;) {
                 const bool have = t < ntiles;
-                const bool reading = (uint64_t)wall_clock64() % period < read_ticks;
+                now = (uint64_t)wall_clock64();
+                while (now - start >= period)
+                    start += period;
+                const bool reading = now - start < read_ticks;
                 if (have && nbuf < cap && reading) {
                     proc(t, buf[k], nbuf);
                     ++nbuf;
