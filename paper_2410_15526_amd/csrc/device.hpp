@@ -322,9 +322,10 @@ SDP4_DEV void fwht_lane(float (&v)[E], float cn)
 // lanes, physical lane p holds element lane el = p ^ (3 * p2) (bits 0 and 1
 // flipped when bit 2 is set; bits 2 and up unchanged; the map is its own
 // inverse).  Element-lane partners el ^ 1, el ^ 2, el ^ 4, el ^ 8 then sit at
-// physical lanes p ^ 1, p ^ 2, p ^ 7, p ^ 8, all reachable by DPP, and every
-// aligned block of 2^k lanes holds the same lanes as before, so group
-// reductions are unchanged.
+// physical lanes p ^ 1, p ^ 2, p ^ 7, p ^ 8, all reachable by DPP, and the
+// element lanes of an aligned block of 2^k lanes sit on one aligned block of
+// physical lanes (the same block for 2^k >= 8), so a group reduction over
+// aligned physical blocks still joins exactly the lanes of each group.
 SDP4_DEV int element_lane(int p)
 {
     const int b = (p >> 2) & 1;
