@@ -5,6 +5,8 @@ Hadamard blocks, groups, peer counts, offsets and value distributions
 magnitudes spanning 1e-30..1e30, exact lattice points) and compares every
 entry point with the oracle.  Examples are derandomized so every GPU run
 draws the same cases."""
+import os
+
 import numpy as np
 import pytest
 
@@ -17,8 +19,10 @@ from tests._gpu import check_codes, check_f32, check_headers, dev, empty, host, 
 
 pytestmark = pytest.mark.gpu
 
-SETTINGS = settings(max_examples=60, deadline=None, derandomize=True, database=None,
-                    suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+# SDP4_FUZZ_EXAMPLES raises the example count for a deeper one-off run (the
+# derandomized sequence is extended, so a failure is reproducible).
+SETTINGS = settings(max_examples=int(os.environ.get("SDP4_FUZZ_EXAMPLES", "60")), deadline=None, derandomize=True,
+                    database=None, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
 DISTS = ["normal", "heavy", "negative", "sparse", "constant_runs", "mixed_magnitude", "lattice"]
 
 
