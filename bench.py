@@ -10,7 +10,8 @@ are seeded synthetic data resident in HBM before timing starts.
 Prints one JSON line.  ``value`` is the fp32-equivalent input throughput of
 the step: 4 bytes x (input elements of every kernel) / step time.  Per
 kernel the line also carries algorithmic HBM bytes / launch time against the
-8 TB/s HBM peak; ``roofline`` is that figure for the kernel that takes the
+8 TB/s HBM peak and against a plain copy kernel measured in the same run
+(``vs_copy``); ``roofline`` is the peak figure for the kernel that takes the
 largest share of the step.  ``cpu_baseline`` is the plain CPU oracle timed
 on a bounded sample of the same workload on this host (single thread).
 
@@ -203,6 +204,7 @@ def main():
         kernels[name] = {"ms": round(ms, 4), "ms_median": round(med, 4), "ms_std": round(std, 4),
                          "alg_bytes": ki.alg_bytes, "alg_GBps": round(alg, 1),
                          "hbm_frac": round(alg / HBM_PEAK_GBPS, 4),
+                         "vs_copy": round(alg / copy_gbps, 4),
                          "fp32_in_GBps": round(ki.fp32_in_bytes / (ms * 1e-3) / 1e9, 1),
                          "elems_per_s": round(ki.fp32_in_bytes / 4 / (ms * 1e-3), 1)}
     dom = max(kernels, key=lambda k: kernels[k]["ms"])
