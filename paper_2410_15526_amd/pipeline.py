@@ -56,6 +56,26 @@ class HotPath:
         self.out_scale = 1.0 / (P * Q)
         self._unfused = None
 
+    def with_groups(self, group: int | None = None, qwd_group: int | None = None) -> "HotPath":
+        """The same data buffers with other group sizes (new header arrays
+        only), for group-size sweeps on one shard."""
+        import copy
+        import torch
+        h = copy.copy(self)
+        e = lambda k: torch.empty(k, dtype=torch.float32, device=self.grad.device)
+        if group is not None and group != self.group:
+            if self.n % (self.P * self.Q * max(group, self.block)):
+                raise ValueError("n must be a multiple of P*Q*max(group, block)")
+            h.group = group
+            h.s8, h.s4 = e(self.n // group), e(self.M // group)
+        if qwd_group is not None and qwd_group != self.qwd_group:
+            if self.n % qwd_group:
+                raise ValueError("n must be a multiple of the qWD group")
+            h.qwd_group = qwd_group
+            h.qscale, h.qmin = e(self.n // qwd_group), e(self.n // qwd_group)
+        h._unfused = None
+        return h
+
     # -- the five launches ---------------------------------------------------
     def qwd_encode(self, stream=None):
         sdp4.sdp4_qwd_encode(self.w_new, self.w_prev, self.qwd_group, self.qcodes, self.qscale, self.qmin,
