@@ -17,9 +17,9 @@
 // chunk per peer), and per kernel family a block shape -- one resident
 // block of four waves per CU for the qWD encoder and decoder, one block of
 // eight waves for K1 (four without a transform) and for the 8-bit K2, two
-// blocks of four waves for the rest.  (How many bytes a CU keeps in flight, and how far compute spreads
-// its requests out, moves the mixed read/write bandwidth of HBM by several
-// per cent.)
+// blocks of four waves for the rest.  (How many bytes a CU keeps in flight,
+// and how far compute spreads its requests out, moves the mixed read/write
+// bandwidth of HBM by several per cent.)
 #pragma once
 
 #include "device.hpp"
@@ -46,7 +46,10 @@
 #define SDP4_E_RED 32
 #endif
 #ifndef SDP4_E_RQ8
-#define SDP4_E_RQ8 16 // re-quantizing dequantize-reduce of 8-bit messages (also stochastically rounded): one 16-byte chunk per peer and lane
+// Elements per lane of the re-quantizing dequantize-reduce of 8-bit messages,
+// deterministic or stochastically rounded (16: one 16-byte chunk per peer and
+// lane; groups up to 1024).
+#define SDP4_E_RQ8 16
 #endif
 #ifndef SDP4_BLOCKS_PER_CU
 #define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
