@@ -1,0 +1,71 @@
+"""Host-side logic of bench.py (no GPU): the one-GPU guard, the use of the
+recorded HBM-traffic summary only for the kernel sources and workload it was
+taken on, the algorithmic byte counts per launch, and the CPU description."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+@pytest.mark.parametrize("argv,env", [(["--gpus", "2"], {}), (["--gpus", "8"], {}), ([], {"WORLD_SIZE": "2"})])
+def test_more_than_one_gpu_exits_with_a_message(argv, env):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv], capture_output=True, text=True,
+                       env={**os.environ, **env}, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_traffic_is_used_only_for_matching_sources_and_workload(tmp_path, monkeypatch):
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    rec = {"source_digest": bench.source_digest(), "workload_key": "c5",
+           "kernels": {"qwd_encode": {"bytes_per_launch": 123}}}
+    (prof / "hbm_traffic.json").write_text(json.dumps(rec))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "source_digest", lambda: rec["source_digest"])
+    assert bench.traffic_for("qwd_encode") == 123
+    assert bench.traffic_for("qwd_encode", "c4") is None            # another workload
+    assert bench.traffic_for("grad_quant") is None                  # no record for that kernel
+    monkeypatch.setattr(bench, "source_digest", lambda: "another")  # kernel sources changed since
+    assert bench.traffic_for("qwd_encode") is None
+    (prof / "hbm_traffic.json").write_text("not json")
+    assert bench.traffic_for("qwd_encode") is None
+
+
+def test_source_digest_covers_device_sources_only(tmp_path, monkeypatch):
+    csrc = tmp_path / "paper_2410_15526_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    (csrc / "kernels.hpp").write_text("a")
+    (csrc / "abi.cpp").write_text("x")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    d0 = bench.source_digest()
+    (csrc / "abi.cpp").write_text("y")              # host-side argument checks only
+    assert bench.source_digest() == d0
+    (csrc / "kernels.hpp").write_text("b")
+    assert bench.source_digest() != d0
+
+
+def test_algorithmic_bytes_per_launch():
+    """The per-element byte counts of the kernels (reads + writes, group 128,
+    bf16 model weights), checked against the c5 shard's launches."""
+    pytest.importorskip("torch")
+    from paper_2410_15526_amd.pipeline import HotPath
+    n, g, P, Q = 1_625_292_800, 128, 8, 4
+    info = HotPath.kernel_info(type("S", (), dict(n=n, group=g, qwd_group=g, P=P, Q=Q, M=n // P, m=n // P // Q,
+                                                   prev_dtype="bf16"))())
+    assert info["qwd_encode"].alg_bytes == n * (4 + 2 + 0.5) + 8 * n // g == 10_665_984_000
+    assert info["qwd_decode"].alg_bytes == 7_415_398_400
+    assert info["grad_quant"].alg_bytes == n * 5 + 4 * n // g == 8_177_254_400
+    assert info["reduce_intra"].alg_bytes == 1_784_012_800
+    assert info["reduce_inter"].alg_bytes == 311_091_200
+
+
+def test_host_cpu_names_model_and_cores():
+    s = bench.host_cpu()
+    assert "cores available" in s and len(s) > len("cores available")
