@@ -11,8 +11,14 @@ int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, in
                  uint8_t *codes, float *scale, float *minv, hipStream_t s)
 {
     constexpr int WPB = kEncWaves;
-    auto k = bf16 ? (sym ? k_qwd_encode<true, true, E, kDepth, WPB> : k_qwd_encode<true, false, E, kDepth, WPB>)
-                  : (sym ? k_qwd_encode<false, true, E, kDepth, WPB> : k_qwd_encode<false, false, E, kDepth, WPB>);
+    // groups of 64 take the instantiation whose header buffer holds 32 per tile
+    auto k = group >= 128 || E != 32
+                 ? (bf16 ? (sym ? k_qwd_encode<true, true, E, kDepth, WPB> : k_qwd_encode<true, false, E, kDepth, WPB>)
+                         : (sym ? k_qwd_encode<false, true, E, kDepth, WPB> : k_qwd_encode<false, false, E, kDepth, WPB>))
+                 : (bf16 ? (sym ? k_qwd_encode<true, true, E, kDepth, WPB, 64>
+                                : k_qwd_encode<true, false, E, kDepth, WPB, 64>)
+                         : (sym ? k_qwd_encode<false, true, E, kDepth, WPB, 64>
+                                : k_qwd_encode<false, false, E, kDepth, WPB, 64>));
     // Read/write phases for large launches with 32 elements per lane and a
     // group of at least kEncPhaseMinGroup; everything else streams as usual.
     uint64_t period = 0, read_ticks = 0;

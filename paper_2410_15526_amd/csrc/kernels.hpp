@@ -114,17 +114,25 @@
 #define SDP4_ENC_PHASE_DEPTH 1 // tiles each phased encoder wave keeps loading ahead
 #endif
 #ifndef SDP4_ENC_PHASE_CAP
-#define SDP4_ENC_PHASE_CAP 27 // tiles of codes and headers each encoder wave buffers in LDS
+#define SDP4_ENC_PHASE_CAP 27 // tiles of codes and headers each encoder wave buffers in LDS (groups >= 128)
+#endif
+#ifndef SDP4_ENC_PHASE_CAP64
+#define SDP4_ENC_PHASE_CAP64 25 // the same for groups of 64
 #endif
 
 namespace sdp4 {
 
 constexpr int kDepth = SDP4_PIPE;
 constexpr int kEncPhaseCap = SDP4_ENC_PHASE_CAP; // tiles buffered per wave by the phased encoder
+constexpr int kEncPhaseCap64 = SDP4_ENC_PHASE_CAP64; // ... when its headers are those of groups of 64
 constexpr int kEncPhaseDepth = SDP4_ENC_PHASE_DEPTH;
 static_assert(SDP4_ENC_READ_PCT > 0 && SDP4_ENC_READ_PCT < 100, "the encoder's read phase is part of its period");
 static_assert(SDP4_ENC_PHASE_CAP >= 1 && SDP4_ENC_PHASE_DEPTH >= 1, "phased encoder buffers");
-constexpr int kEncPhaseMinGroup = 128;      // smallest group the phased encoder buffers headers for
+constexpr int kEncPhaseMinGroup = 64;       // smallest group the phased encoder buffers headers for
+// Tiles buffered per wave for a given smallest group: headers for groups of 64
+// take twice the room of those for groups of 128 and up, and the buffers of
+// four waves must fit the 160 KiB of LDS.
+constexpr int enc_phase_cap(int min_group) { return min_group >= 128 ? kEncPhaseCap : kEncPhaseCap64; }
 constexpr int64_t kPhaseMinElements = 1 << 26; // smaller launches use the ordinary stream
 
 // Persistent loop of one wavefront over its tiles t, t + S, t + 2S, ...
@@ -284,7 +292,7 @@ SDP4_DEV void fused_fwht(float (&v)[E], float cn, int el)
 // (codes 0..15, scale and minimum) or, with SYM, symmetric (codes -7..7,
 // scale only; minv is not touched)
 // ---------------------------------------------------------------------------
-template <bool BF16, bool SYM, int E, int DEPTH, int WPB>
+template <bool BF16, bool SYM, int E, int DEPTH, int WPB, int PMIN = 128>
 __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     const float *__restrict__ w_new, const void *__restrict__ w_prev, int64_t n, int group,
     uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv, uint64_t period,
@@ -294,10 +302,11 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     constexpr int R = E / 4;                       // f32 chunks per lane
     constexpr int RP = BF16 ? E / 8 : E / 4;       // previous-weight chunks per lane
     // Phased mode (E = 32: one 16-byte code chunk per lane and tile) buffers
-    // CAP tiles per wave: codes, then scales and minima of up to HMAX groups.
+    // CAP tiles per wave: codes, then scales and minima of up to HMAX groups
+    // (groups of at least PMIN elements).
     constexpr bool PHASED = E == 32;
-    constexpr int CAP = PHASED ? kEncPhaseCap : 1;
-    constexpr int HMAX = W / kEncPhaseMinGroup;
+    constexpr int CAP = PHASED ? enc_phase_cap(PMIN) : 1;
+    constexpr int HMAX = W / PMIN;
     __shared__ u32x4 lds_all[WPB][kWave * R];
     __shared__ u32x4 cbuf_all[WPB][CAP * kWave];
     __shared__ float hbuf_all[WPB][CAP * 2 * HMAX];
@@ -393,7 +402,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
         tile_loop<DEPTH, WPB, Tile>(ntiles, load, proc);
         return;
     }
-    if constexpr (PHASED) { // group >= kEncPhaseMinGroup (the launcher checks)
+    if constexpr (PHASED) { // group >= PMIN (the launcher checks)
         u32x4 *cbuf = cbuf_all[wv];
         float *hbuf = hbuf_all[wv];
         int64_t *tbuf = tbuf_all[wv];
