@@ -115,6 +115,10 @@ extern "C" {
  *   minv    [n/group] float32  out: minimum of each group
  * Inputs are not modified.  Errors: EINVAL (null, bad group or dtype,
  * overlap of an output with an input), EALIGN, EHIP.
+ * Large launches (n >= 2^26, group >= 64) pace their memory traffic by the
+ * device's constant-rate wall clock: every wave reads in one part of a
+ * fixed period and writes its buffered output in the rest.  The outputs do
+ * not depend on the timing; other work on the same GPU only slows the call.
  */
 int sdp4_qwd_encode(const float *w_new, const void *w_prev, int prev_dtype, int64_t n, int group,
                     uint8_t *codes, float *scale, float *minv, void *stream);
@@ -146,7 +150,8 @@ int sdp4_qwd_decode(const uint8_t *codes, const float *scale, const float *minv,
  *                              (even element in the low nibble; -8 unused)
  *   scale   [n/group] float32  out: s / 7 of each group
  * The message is 4 + 32/group bits per element (no minimum).  Inputs are
- * not modified.  Errors: EINVAL, EALIGN, EHIP as for sdp4_qwd_encode.
+ * not modified.  Errors: EINVAL, EALIGN, EHIP as for sdp4_qwd_encode, and
+ * large launches are paced by the wall clock in the same way.
  */
 int sdp4_qwd_encode_sym(const float *w_new, const void *w_prev, int prev_dtype, int64_t n, int group,
                         uint8_t *codes, float *scale, void *stream);
