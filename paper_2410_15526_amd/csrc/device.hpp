@@ -172,6 +172,29 @@ SDP4_DEV void transpose_in(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R])
     transpose_in<R>(t, lds, out, lane_id());
 }
 
+// The same through an LDS region of half the tile (32*R chunks): lanes
+// 0..31 take their chunks from the first half of the coalesced chunks,
+// lanes 32..63 from the second, one half after the other.
+template <int R>
+SDP4_DEV void transpose_in_halves(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R])
+{
+    static_assert(R % 2 == 0, "halves");
+    const int lane = lane_id();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int i = 0; i < R / 2; ++i)
+            lds[swz<R>(kWave * i + lane)] = t[h * (R / 2) + i];
+        wave_lds_sync();
+        if ((lane >> 5) == h) {
+#pragma unroll
+            for (int k = 0; k < R; ++k)
+                out[k] = lds[swz<R>(R * (lane & 31) + k)];
+        }
+        wave_lds_sync();
+    }
+}
+
 // Global (coalesced) -> registers (lane-contiguous).
 template <int R>
 SDP4_DEV void stage_in(const u32x4 *__restrict__ g, int valid, u32x4 *lds, u32x4 (&out)[R])

@@ -27,7 +27,10 @@ int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, in
         const int khz = wall_clock_khz(err);
         if (err != hipSuccess)
             return set_hip_error(err);
-        period = khz > 0 ? (uint64_t)khz * SDP4_ENC_PHASE_US / 1000 : 0;
+        // the period is set for the buffer of groups >= 128 and scales with
+        // the buffer of the instantiation that runs
+        const int cap = enc_phase_cap(group >= 128 ? 128 : 64);
+        period = khz > 0 ? (uint64_t)khz * SDP4_ENC_PHASE_US * cap / (1000 * enc_phase_cap(128)) : 0;
         read_ticks = period * SDP4_ENC_READ_PCT / 100;
         // Both phases must last at least one clock tick, or a wave could wait
         // for a phase that never comes: otherwise stream.

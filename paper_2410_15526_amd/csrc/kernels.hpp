@@ -105,19 +105,22 @@
 #endif
 
 #ifndef SDP4_ENC_PHASE_US
-#define SDP4_ENC_PHASE_US 50 // qWD encoder read/write period in microseconds (0: ordinary stream)
+#define SDP4_ENC_PHASE_US 68 // qWD encoder read/write period in microseconds (0: ordinary stream)
 #endif
 #ifndef SDP4_ENC_READ_PCT
-#define SDP4_ENC_READ_PCT 90 // per cent of the period spent reading
+#define SDP4_ENC_READ_PCT 92 // per cent of the period spent reading
 #endif
 #ifndef SDP4_ENC_PHASE_DEPTH
 #define SDP4_ENC_PHASE_DEPTH 1 // tiles each phased encoder wave keeps loading ahead
 #endif
+#ifndef SDP4_ENC_HALF_T
+#define SDP4_ENC_HALF_T 1 // encoder: transpose its inputs through an LDS region of half a tile
+#endif
 #ifndef SDP4_ENC_PHASE_CAP
-#define SDP4_ENC_PHASE_CAP 27 // tiles of codes and headers each encoder wave buffers in LDS (groups >= 128)
+#define SDP4_ENC_PHASE_CAP (SDP4_ENC_HALF_T ? 31 : 27) // tiles each encoder wave buffers in LDS (groups >= 128)
 #endif
 #ifndef SDP4_ENC_PHASE_CAP64
-#define SDP4_ENC_PHASE_CAP64 25 // the same for groups of 64
+#define SDP4_ENC_PHASE_CAP64 (SDP4_ENC_HALF_T ? 28 : 25) // the same for groups of 64
 #endif
 
 namespace sdp4 {
@@ -307,7 +310,9 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     constexpr bool PHASED = E == 32;
     constexpr int CAP = PHASED ? enc_phase_cap(PMIN) : 1;
     constexpr int HMAX = W / PMIN;
-    __shared__ u32x4 lds_all[WPB][kWave * R];
+    // inputs of 8 chunks per lane pass through the LDS in two halves
+    constexpr bool HALFT = SDP4_ENC_HALF_T && R == 8;
+    __shared__ u32x4 lds_all[WPB][kWave * (HALFT ? R / 2 : R)];
     __shared__ u32x4 cbuf_all[WPB][CAP * kWave];
     __shared__ float hbuf_all[WPB][CAP * 2 * HMAX];
     __shared__ int64_t tbuf_all[WPB][CAP];
@@ -338,12 +343,18 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
         float d[E], p[E];
         {
             u32x4 c[R];
-            transpose_in<R>(in.a, lds, c);
+            if constexpr (HALFT)
+                transpose_in_halves<R>(in.a, lds, c);
+            else
+                transpose_in<R>(in.a, lds, c);
             chunks_to_f32<E>(c, d);
         }
         {
             u32x4 c[RP];
-            transpose_in<RP>(in.b, lds, c);
+            if constexpr (HALFT && RP == R)
+                transpose_in_halves<RP>(in.b, lds, c);
+            else
+                transpose_in<RP>(in.b, lds, c);
             if constexpr (BF16)
                 bf16_chunks_to_f32<E>(c, p);
             else
