@@ -13,7 +13,9 @@ kernel the line also carries algorithmic HBM bytes / launch time against the
 8 TB/s HBM peak and against a plain copy kernel measured in the same run
 (``vs_copy``); ``roofline`` is the peak figure for the kernel that takes the
 largest share of the step.  ``cpu_baseline`` is the plain CPU oracle timed
-on a bounded sample of the same workload on this host (single thread).
+on a bounded sample of the same workload on this host (single thread);
+``cpu_baseline_all_cores`` the same oracle on the same sample split into one
+slice per available core (up to 16), each in its own thread.
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 20] [--workload c5]
 """
@@ -98,18 +100,18 @@ def host_cpu() -> str:
     return f"{name}, {len(os.sched_getaffinity(0))} cores available"
 
 
-def cpu_baseline(w, sample_log2: int, seed: int):
-    """The oracle on a contiguous sample of the workload: one full step."""
-    import numpy as np
-    import oracle
+def _oracle_inputs(w, lo: int, n: int, seed: int):
     import synth
-    n = 1 << sample_log2
+    return (synth.prev_weights(w, lo, n, seed), synth.new_weights(w, lo, n, seed), synth.gradient(w, lo, n, seed))
+
+
+def _oracle_step(w, prev, new, grad):
+    """One full step of the oracle on one contiguous slice (its own chain:
+    the slice's P chunks are the peers of the 8-bit reduction, and so on)."""
+    import oracle
+    n = prev.size
     P, Q, g, hb, qg = w.P, w.Q, w.group, w.hadamard_block, w.qwd_group
-    prev = synth.prev_weights(w, 0, n, seed)
-    new = synth.new_weights(w, 0, n, seed)
-    grad = synth.gradient(w, 0, n, seed)
     M, m = n // P, n // P // Q
-    t0 = time.perf_counter()
     c, s, mn, _ = oracle.qwd_encode(new, prev, qg)
     oracle.qwd_decode(c, s, mn, prev, qg)
     k1c, k1s, _ = oracle.grad_quant(grad, 8, hb, g)
@@ -118,13 +120,53 @@ def cpu_baseline(w, sample_log2: int, seed: int):
     oracle.dequant_reduce([r["codes"][q * m // 2:(q + 1) * m // 2] for q in range(Q)],
                           [r["scales"][q * m // g:(q + 1) * m // g] for q in range(Q)], m, 4, g, 0, hb,
                           1.0 / (P * Q))
+
+
+def _step_fp32_bytes(w, n: int) -> int:
+    return 4 * (n + n + n + n + n // w.P)
+
+
+def _step_desc(w) -> str:
+    return (f"one full step (qWD encode+decode, Hadamard+8-bit, 8-bit x{w.P} reduce + 4-bit, 4-bit x{w.Q} "
+            f"reduce + inverse Hadamard)")
+
+
+def cpu_baseline(w, sample_log2: int, seed: int):
+    """The oracle on a contiguous sample of the workload: one full step."""
+    n = 1 << sample_log2
+    prev, new, grad = _oracle_inputs(w, 0, n, seed)
+    t0 = time.perf_counter()
+    _oracle_step(w, prev, new, grad)
     dt = time.perf_counter() - t0
-    fp32_bytes = 4 * (n + n + n + n + n // P)
-    return {"value": round(fp32_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    return {"value": round(_step_fp32_bytes(w, n) / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "seconds": round(dt, 3), "host_cpu": host_cpu(),
-            "sample": f"elements [0, 2^{sample_log2}) of the same workload, one full step "
-                      f"(qWD encode+decode, Hadamard+8-bit, 8-bit x{P} reduce + 4-bit, 4-bit x{Q} reduce + "
-                      f"inverse Hadamard), single-threaded plain C oracle"}
+            "sample": f"elements [0, 2^{sample_log2}) of the same workload, {_step_desc(w)}, single-threaded "
+                      f"plain C oracle"}
+
+
+def cpu_baseline_all_cores(w, sample_log2: int, seed: int, max_threads: int = 16):
+    """The same oracle on the same sample, split into one contiguous slice per
+    available core (at most max_threads), each slice a full step of its own in
+    its own thread (the oracle's C calls release the interpreter lock).
+    Groups and blocks are independent, so every slice computes exactly what
+    the single-threaded run computes for those elements."""
+    import concurrent.futures as cf
+    import math
+    n = 1 << sample_log2
+    T = max(1, min(len(os.sched_getaffinity(0)), max_threads))
+    unit = w.P * w.Q * math.lcm(w.group, w.hadamard_block or 1, w.qwd_group)
+    per = n // T // unit * unit
+    if per == 0:
+        T, per = 1, n
+    slices = [_oracle_inputs(w, i * per, per, seed) for i in range(T)]
+    with cf.ThreadPoolExecutor(T) as ex:
+        t0 = time.perf_counter()
+        list(ex.map(lambda a: _oracle_step(w, *a), slices))
+        dt = time.perf_counter() - t0
+    return {"value": round(_step_fp32_bytes(w, per) * T / dt / 1e9, 4), "unit": "GB/s", "cores": T,
+            "kind": "oracle", "seconds": round(dt, 3), "host_cpu": host_cpu(),
+            "sample": f"elements [0, {T * per}) of the same workload in {T} slices of {per}, {_step_desc(w)} "
+                      f"per slice, one thread per slice, plain C oracle"}
 
 
 def main():
@@ -349,6 +391,8 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample ...")
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_log2, args.seed)
+        log("timing the CPU oracle on all cores ...")
+        line["cpu_baseline_all_cores"] = cpu_baseline_all_cores(w, args.cpu_sample_log2, args.seed)
     print(json.dumps(line), flush=True)
 
 

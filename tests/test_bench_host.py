@@ -69,3 +69,16 @@ def test_algorithmic_bytes_per_launch():
 def test_host_cpu_names_model_and_cores():
     s = bench.host_cpu()
     assert "cores available" in s and len(s) > len("cores available")
+
+
+def test_all_cores_baseline_slices_the_sample(monkeypatch):
+    """The all-cores oracle leg: whole-step slices of the sample, each a
+    multiple of every group, block and chunk size, one thread per core."""
+    pytest.importorskip("numpy")
+    import synth
+    w = synth.WORKLOADS["c5"]
+    monkeypatch.setattr(bench.os, "sched_getaffinity", lambda pid: set(range(3)))
+    r = bench.cpu_baseline_all_cores(w, 16, 0)
+    assert r["cores"] == 3 and r["kind"] == "oracle" and r["value"] > 0
+    per = int(r["sample"].split(" slices of ")[1].split(",")[0])
+    assert per % (w.P * w.Q * max(w.group, w.hadamard_block, w.qwd_group)) == 0 and 3 * per <= 1 << 16
