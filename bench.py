@@ -181,6 +181,7 @@ def main():
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--no-table5", action="store_true")
+    ap.add_argument("--no-standalone", action="store_true")
     ap.add_argument("--no-group-sweep", action="store_true")
     args = ap.parse_args()
 
@@ -337,7 +338,7 @@ def main():
     # Hadamard transform (the size the paper uses), group 128; GB/s of fp32 input / output
     table5 = {}
     if not args.no_table5:
-        del hp
+        hp = None  # the step's buffers are no longer needed
         torch.cuda.empty_cache()
         for mb in (8, 16, 64, 512, 1024, 2048):
             n = mb * (1 << 20) // 4
@@ -355,6 +356,28 @@ def main():
                 row[f"dequant_{tag}_GBps"] = round(4 * n / (t_d * 1e-3) / 1e9, 1)
             table5[f"{mb}MB"] = row
             del x, c, s, y
+
+    # K3 standalone on N_in = N (the workload's element count) 4-bit inputs: Q chunks of N/Q
+    # elements reduced into N/Q fp32 outputs with the inverse Hadamard transform (in the chain K3 gets
+    # only N/P of them, too few launches' worth of tiles to reach the steady rate)
+    standalone = {}
+    if not args.no_standalone:
+        hp = None  # the step's buffers are no longer needed
+        torch.cuda.empty_cache()
+        m, g, Q = w.n // w.Q, w.group, w.Q
+        gen = torch.Generator(device="cuda").manual_seed(args.seed)
+        c4 = torch.randint(0, 256, (Q * m // 2,), dtype=torch.uint8, device="cuda", generator=gen)
+        s4 = torch.rand(Q * m // g, device="cuda", generator=gen) * 1e-3
+        out = torch.empty(m, device="cuda")
+        cl = [c4[q * m // 2:(q + 1) * m // 2] for q in range(Q)]
+        sl = [s4[q * m // g:(q + 1) * m // g] for q in range(Q)]
+        ms = timed(lambda: sdp4.sdp4_dequant_reduce(cl, sl, m, 4, g, 0, w.hadamard_block, 1.0 / (w.P * Q), None,
+                                                    None, out), reps=20)
+        alg = Q * (m // 2 + 4 * (m // g)) + 4 * m
+        gbps = alg / (ms * 1e-3) / 1e9
+        standalone["reduce_inter"] = {"n_in": Q * m, "ms": ms, "alg_bytes": alg, "alg_GBps": round(gbps, 1),
+                                      "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+        del c4, s4, out, cl, sl
 
     traffic = traffic_for(dom, args.workload)
     line = {
@@ -386,6 +409,8 @@ def main():
         line["variants"] = variants
     if table5:
         line["table5_sweep"] = table5
+    if standalone:
+        line["standalone"] = standalone
     if group_sweep:
         line["group_sweep"] = group_sweep
     if not args.no_cpu_baseline:
