@@ -13,8 +13,12 @@
 // Global memory is read and written in the coalesced order (instruction i,
 // lane l touches the 16-byte chunk 64*i + l of the tile) and transposed to
 // or from the lane-contiguous layout through a wave-private LDS region, with
-// an XOR swizzle of the chunk index so that both the coalesced and the
-// transposed access patterns are free of LDS bank conflicts.
+// an XOR swizzle of the chunk index that keeps both access patterns of each
+// transpose free of LDS bank conflicts.  The LDS serves a 16-byte read to 16
+// lanes per cycle over 64 banks of 4 bytes, a 16-byte write to 8 lanes over
+// 32 (as the bank-conflict counters show), so a transpose in (coalesced
+// write, lane-contiguous read) and a transpose out (lane-contiguous write,
+// coalesced read) take different swizzles.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -116,7 +120,11 @@ SDP4_DEV void minmax_lanes(float &mn, float &mx, int lanes)
 // ---------------------------------------------------------------------------
 // LDS staging between the coalesced and the lane-contiguous layouts
 // ---------------------------------------------------------------------------
-// R = 16-byte chunks per lane; the wave tile has 64*R chunks.
+// R = 16-byte chunks per lane; the wave tile has 64*R chunks.  Both
+// swizzles permute chunks within aligned blocks of R (or 8) chunks.
+//
+// Transpose out: lanes l .. l+7 write chunks R*l + k (rows R apart) and
+// lanes l .. l+15 read the consecutive chunks c .. c+15.
 template <int R>
 SDP4_DEV int swz(int c)
 {
@@ -124,6 +132,17 @@ SDP4_DEV int swz(int c)
         return c ^ ((c / R) & 7);
     else
         return c ^ ((c >> 3) & 7);
+}
+
+// Transpose in: lanes l .. l+7 write consecutive chunks and lanes
+// l .. l+15 read chunks R*l + k, whose bits 4 and up hold the lane's low
+// bits; folding them into the chunk's low bits spreads the 16 reads over
+// the 16 bank quads.
+template <int R>
+SDP4_DEV int swz_in(int c)
+{
+    static_assert(R >= 1 && R <= 16 && (R & (R - 1)) == 0, "chunks per lane");
+    return c ^ ((c >> 4) & (R - 1));
 }
 
 // Coalesced global loads of one tile: instruction i, lane l reads chunk
@@ -158,11 +177,11 @@ SDP4_DEV void transpose_in(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[R], int
     const int lane = lane_id();
 #pragma unroll
     for (int i = 0; i < R; ++i)
-        lds[swz<R>(kWave * i + lane)] = t[i];
+        lds[swz_in<R>(kWave * i + lane)] = t[i];
     wave_lds_sync();
 #pragma unroll
     for (int k = 0; k < R; ++k)
-        out[k] = lds[swz<R>(R * el + k)];
+        out[k] = lds[swz_in<R>(R * el + k)];
     wave_lds_sync();
 }
 
@@ -184,12 +203,12 @@ SDP4_DEV void transpose_in_halves(const u32x4 (&t)[R], u32x4 *lds, u32x4 (&out)[
     for (int h = 0; h < 2; ++h) {
 #pragma unroll
         for (int i = 0; i < R / 2; ++i)
-            lds[swz<R>(kWave * i + lane)] = t[h * (R / 2) + i];
+            lds[swz_in<R>(kWave * i + lane)] = t[h * (R / 2) + i];
         wave_lds_sync();
         if ((lane >> 5) == h) {
 #pragma unroll
             for (int k = 0; k < R; ++k)
-                out[k] = lds[swz<R>(R * (lane & 31) + k)];
+                out[k] = lds[swz_in<R>(R * (lane & 31) + k)];
         }
         wave_lds_sync();
     }
