@@ -80,6 +80,28 @@ def _ptr(x):
     return x.data_ptr()
 
 
+def _need(x, nbytes: int, what: str) -> None:
+    """A tensor argument must hold every byte the call reads or writes
+    through it: the library sees only its address, so a short tensor would
+    be overrun on the device.  Integer addresses are the caller's to size."""
+    if x is None or isinstance(x, int):
+        return
+    have = x.numel() * x.element_size()
+    if have < nbytes:
+        raise ValueError(f"sdp4: {what} holds {have} bytes; the call touches {nbytes}")
+
+
+def _ng(n: int, group: int) -> int:
+    """Groups in n elements; 0 for a group the library will reject itself."""
+    ok = isinstance(group, int) and group > 0 and group & (group - 1) == 0
+    return n // group if ok else 0
+
+
+def _prev_bytes(w_prev, n: int) -> int:
+    import torch
+    return (4 if w_prev.dtype == torch.float32 else 2) * n
+
+
 def _stream(stream):
     if stream is None:
         import torch
@@ -106,6 +128,8 @@ def _ck(name: str, rc: int) -> None:
 def sdp4_qwd_encode(w_new, w_prev, group, codes, scale, minv, n=None, stream=None):
     """codes/scale/minv <- 4-bit quantized (w_new - w_prev); see include/sdp4.h."""
     n = w_new.numel() if n is None else n
+    _need(w_new, 4 * n, "w_new"); _need(w_prev, _prev_bytes(w_prev, n), "w_prev"); _need(codes, n // 2, "codes")
+    _need(scale, 4 * _ng(n, group), "scale"); _need(minv, 4 * _ng(n, group), "minv")
     _ck("sdp4_qwd_encode", lib().sdp4_qwd_encode(_ptr(w_new), _ptr(w_prev), _prev_dtype(w_prev), n, group,
                                                  _ptr(codes), _ptr(scale), _ptr(minv), _stream(stream)))
 
@@ -113,6 +137,8 @@ def sdp4_qwd_encode(w_new, w_prev, group, codes, scale, minv, n=None, stream=Non
 def sdp4_qwd_decode(codes, scale, minv, group, w_prev, n=None, stream=None):
     """w_prev <- w_prev + dequantized message, in place."""
     n = w_prev.numel() if n is None else n
+    _need(codes, n // 2, "codes"); _need(scale, 4 * _ng(n, group), "scale"); _need(minv, 4 * _ng(n, group), "minv")
+    _need(w_prev, _prev_bytes(w_prev, n), "w_prev")
     _ck("sdp4_qwd_decode", lib().sdp4_qwd_decode(_ptr(codes), _ptr(scale), _ptr(minv), n, group,
                                                  _ptr(w_prev), _prev_dtype(w_prev), _stream(stream)))
 
@@ -120,6 +146,8 @@ def sdp4_qwd_decode(codes, scale, minv, group, w_prev, n=None, stream=None):
 def sdp4_qwd_encode_sym(w_new, w_prev, group, codes, scale, n=None, stream=None):
     """codes/scale <- symmetric 4-bit quantized (w_new - w_prev); see include/sdp4.h."""
     n = w_new.numel() if n is None else n
+    _need(w_new, 4 * n, "w_new"); _need(w_prev, _prev_bytes(w_prev, n), "w_prev"); _need(codes, n // 2, "codes")
+    _need(scale, 4 * _ng(n, group), "scale")
     _ck("sdp4_qwd_encode_sym", lib().sdp4_qwd_encode_sym(_ptr(w_new), _ptr(w_prev), _prev_dtype(w_prev), n, group,
                                                          _ptr(codes), _ptr(scale), _stream(stream)))
 
@@ -127,14 +155,26 @@ def sdp4_qwd_encode_sym(w_new, w_prev, group, codes, scale, n=None, stream=None)
 def sdp4_qwd_decode_sym(codes, scale, group, w_prev, n=None, stream=None):
     """w_prev <- w_prev + dequantized symmetric message, in place."""
     n = w_prev.numel() if n is None else n
+    _need(codes, n // 2, "codes"); _need(scale, 4 * _ng(n, group), "scale"); _need(w_prev, _prev_bytes(w_prev, n), "w_prev")
     _ck("sdp4_qwd_decode_sym", lib().sdp4_qwd_decode_sym(_ptr(codes), _ptr(scale), n, group, _ptr(w_prev),
                                                          _prev_dtype(w_prev), _stream(stream)))
 
 
 def sdp4_grad_quant(x, bits, hadamard_block, group, codes, scale, n=None, stream=None):
     n = x.numel() if n is None else n
+    _need(x, 4 * n, "x"); _need(codes, n * bits // 8, "codes"); _need(scale, 4 * _ng(n, group), "scale")
     _ck("sdp4_grad_quant", lib().sdp4_grad_quant(_ptr(x), n, bits, hadamard_block, group, _ptr(codes),
                                                  _ptr(scale), _stream(stream)))
+
+
+def _need_reduce(codes, scales, n_chunk, bits_in, group, bits_out, out_codes, out_scales, out_f32):
+    for p, (c, sc) in enumerate(zip(codes, scales)):
+        _need(c, n_chunk * bits_in // 8, f"codes[{p}]")
+        _need(sc, 4 * _ng(n_chunk, group), f"scales[{p}]")
+    if bits_out:
+        _need(out_codes, n_chunk * bits_out // 8, "out_codes")
+        _need(out_scales, 4 * _ng(n_chunk, group), "out_scales")
+    _need(out_f32, 4 * n_chunk, "out_f32")
 
 
 def sdp4_dequant_reduce(codes, scales, n_chunk, bits_in, group, bits_out, hadamard_block=0,
@@ -143,6 +183,7 @@ def sdp4_dequant_reduce(codes, scales, n_chunk, bits_in, group, bits_out, hadama
     P = len(codes)
     if len(scales) != P:
         raise ValueError("sdp4_dequant_reduce: codes and scales differ in length")
+    _need_reduce(codes, scales, n_chunk, bits_in, group, bits_out, out_codes, out_scales, out_f32)
     cp = (C.c_void_p * max(P, 1))(*[_ptr(c) for c in codes])
     sp = (C.c_void_p * max(P, 1))(*[_ptr(s) for s in scales])
     _ck("sdp4_dequant_reduce", lib().sdp4_dequant_reduce(
@@ -154,6 +195,7 @@ def sdp4_dequant_reduce(codes, scales, n_chunk, bits_in, group, bits_out, hadama
 def sdp4_grad_quant_sr(x, bits, hadamard_block, group, seed, offset, codes, scale, n=None, stream=None):
     """Stochastically rounded sdp4_grad_quant (unbiased; see include/sdp4.h)."""
     n = x.numel() if n is None else n
+    _need(x, 4 * n, "x"); _need(codes, n * bits // 8, "codes"); _need(scale, 4 * _ng(n, group), "scale")
     _ck("sdp4_grad_quant_sr", lib().sdp4_grad_quant_sr(_ptr(x), n, bits, hadamard_block, group, seed, offset,
                                                        _ptr(codes), _ptr(scale), _stream(stream)))
 
@@ -163,6 +205,7 @@ def sdp4_dequant_reduce_sr(codes, scales, n_chunk, bits_in, group, bits_out, see
     P = len(codes)
     if len(scales) != P:
         raise ValueError("sdp4_dequant_reduce_sr: codes and scales differ in length")
+    _need_reduce(codes, scales, n_chunk, bits_in, group, bits_out, out_codes, out_scales, out_f32)
     cp = (C.c_void_p * max(P, 1))(*[_ptr(c) for c in codes])
     sp = (C.c_void_p * max(P, 1))(*[_ptr(s) for s in scales])
     _ck("sdp4_dequant_reduce_sr", lib().sdp4_dequant_reduce_sr(
@@ -172,11 +215,15 @@ def sdp4_dequant_reduce_sr(codes, scales, n_chunk, bits_in, group, bits_out, see
 
 def sdp4_hadamard(x, y, block, n=None, stream=None):
     n = x.numel() if n is None else n
+    _need(x, 4 * n, "x"); _need(y, 4 * n, "y")
     _ck("sdp4_hadamard", lib().sdp4_hadamard(_ptr(x), _ptr(y), n, block, _stream(stream)))
 
 
 def sdp4_reduce_f32(xs, y, n=None, stream=None):
     n = y.numel() if n is None else n
+    for i, x in enumerate(xs):
+        _need(x, 4 * n, f"xs[{i}]")
+    _need(y, 4 * n, "y")
     xp = (C.c_void_p * max(len(xs), 1))(*[_ptr(x) for x in xs])
     _ck("sdp4_reduce_f32", lib().sdp4_reduce_f32(len(xs), C.cast(xp, C.c_void_p), _ptr(y), n,
                                                  _stream(stream)))
@@ -184,6 +231,7 @@ def sdp4_reduce_f32(xs, y, n=None, stream=None):
 
 def sdp4_copy_f32(x, y, n=None, stream=None):
     n = x.numel() if n is None else n
+    _need(x, 4 * n, "x"); _need(y, 4 * n, "y")
     _ck("sdp4_copy_f32", lib().sdp4_copy_f32(_ptr(x), _ptr(y), n, _stream(stream)))
 
 

@@ -238,3 +238,71 @@ def test_header_is_c99_and_a_c_program_links(tmp_path):
     subprocess.run(cmd, check=True, capture_output=True)
     out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
     assert out[:10] == ["1", "2", "0", "3", "1", "2", "2048", "32", "peer count out of range", "0"]
+
+
+class _DevTensor:
+    """Stands in for a device tensor on a machine without a GPU: an address
+    and a size, nothing the library could dereference here."""
+    def __init__(self, nbytes, itemsize=1, f32=False):
+        import torch
+        self._n, self._item = nbytes // itemsize, itemsize
+        self.dtype = torch.float32 if f32 else torch.bfloat16
+        self.is_cuda = True
+
+    def numel(self):
+        return self._n
+
+    def element_size(self):
+        return self._item
+
+    def is_contiguous(self):
+        return True
+
+    def data_ptr(self):
+        return 1 << 40
+
+
+def _binding_calls(monkeypatch):
+    """Replace the library with a recorder: a call that gets through the
+    binding's checks is recorded instead of launched."""
+    calls = []
+
+    class Rec:
+        def __getattr__(self, name):
+            return lambda *a: calls.append(name) or 0
+    monkeypatch.setattr(sdp4, "lib", lambda: Rec())
+    monkeypatch.setattr(sdp4, "_stream", lambda s: None)
+    return calls
+
+
+def test_binding_refuses_tensors_too_small_for_the_call(monkeypatch):
+    """The library sees only addresses: the binding checks that every tensor
+    holds the bytes the call touches, before anything reaches the device."""
+    pytest.importorskip("torch")
+    calls = _binding_calls(monkeypatch)
+    n, g = 1 << 12, 128
+    T = _DevTensor
+    ok = dict(w_new=T(4 * n, 4, True), w_prev=T(2 * n, 2), group=g, codes=T(n // 2), scale=T(4 * n // g, 4),
+              minv=T(4 * n // g, 4))
+    sdp4.sdp4_qwd_encode(**ok)
+    for key, short in (("w_new", T(4 * n - 4, 4, True)), ("w_prev", T(2 * n - 2, 2)), ("codes", T(n // 2 - 1)),
+                       ("scale", T(4 * n // g - 4, 4)), ("minv", T(4 * n // g - 4, 4))):
+        with pytest.raises(ValueError, match=key):
+            sdp4.sdp4_qwd_encode(**{**ok, key: short}, n=n)
+    with pytest.raises(ValueError, match="w_prev"):             # float32 weights take 4 bytes each
+        sdp4.sdp4_qwd_decode(T(n // 2), T(4 * n // g, 4), T(4 * n // g, 4), g, T(2 * n, 4, True), n=n)
+    sdp4.sdp4_grad_quant(T(4 * n, 4, True), 8, 256, g, T(n), T(4 * n // g, 4))
+    with pytest.raises(ValueError, match="codes"):
+        sdp4.sdp4_grad_quant(T(4 * n, 4, True), 8, 256, g, T(n // 2), T(4 * n // g, 4))
+    P, m = 4, n // 4
+    cs, ss = [T(m) for _ in range(P)], [T(4 * m // g, 4) for _ in range(P)]
+    sdp4.sdp4_dequant_reduce(cs, ss, m, 8, g, 4, 0, 1.0, T(m // 2), T(4 * m // g, 4), None)
+    with pytest.raises(ValueError, match=r"codes\[2\]"):
+        sdp4.sdp4_dequant_reduce(cs[:2] + [T(m // 2)] + cs[3:], ss, m, 8, g, 4, 0, 1.0, T(m // 2), T(4 * m // g, 4))
+    with pytest.raises(ValueError, match="out_f32"):
+        sdp4.sdp4_dequant_reduce(cs, ss, m, 8, g, 0, 256, 1.0, None, None, T(4 * m - 4, 4, True))
+    with pytest.raises(ValueError, match="y"):
+        sdp4.sdp4_copy_f32(T(4 * n, 4, True), T(2 * n, 4, True))
+    with pytest.raises(ValueError, match=r"xs\[1\]"):
+        sdp4.sdp4_reduce_f32([T(4 * n, 4, True), T(4 * n - 4, 4, True)], T(4 * n, 4, True))
+    assert calls == ["sdp4_qwd_encode", "sdp4_grad_quant", "sdp4_dequant_reduce"]
