@@ -20,6 +20,9 @@
  *             which are host arrays of device pointers read during the call
  *             only.  The caller owns every buffer; the library allocates
  *             nothing, frees nothing and keeps no state between calls.
+ *             The library sees addresses only: every buffer must hold
+ *             the bytes its call touches (given with each entry point);
+ *             a shorter one is overrun on the device.
  *  Streams    `stream` is a hipStream_t (NULL = the default stream).  Calls
  *             enqueue their kernels and return; results are visible after
  *             the usual stream synchronization.  Calls are thread-safe.
