@@ -312,6 +312,17 @@ def main():
         del codes, sc, mn, zero
         variants["qwd_sym_encode_ms"] = timed(hp.qwd_encode_sym)
         variants["qwd_sym_decode_ms"] = timed(hp.qwd_decode_sym)
+        if w.prev_dtype == "bf16":
+            # the same shard with float32 model weights: 8.5 bytes per element + 8 per group, each way
+            wf = hp.w_prev.float()
+            qg = w.qwd_group
+            ms_e = timed(lambda: sdp4.sdp4_qwd_encode(hp.w_new, wf, qg, hp.qcodes, hp.qscale, hp.qmin))
+            ms_d = timed(lambda: sdp4.sdp4_qwd_decode(hp.qcodes, hp.qscale, hp.qmin, qg, wf))
+            alg = w.n * 17 // 2 + 8 * (w.n // qg)
+            variants["qwd_f32_encode_ms"], variants["qwd_f32_decode_ms"] = ms_e, ms_d
+            variants["qwd_f32_hbm_frac"] = {"encode": round(alg / (ms_e * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                            "decode": round(alg / (ms_d * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+            del wf
 
     # group-size sweep of the workload (the GPT-6.7B shard sweeps the gradient group 32..512 and
     # the qWD group 64..256): the same data, new header arrays; each kernel timed on its own

@@ -22,7 +22,9 @@ int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, in
     // Read/write phases for large launches with 32 elements per lane and a
     // group of at least kEncPhaseMinGroup; everything else streams as usual.
     uint64_t period = 0, read_ticks = 0;
-    if (E == 32 && SDP4_ENC_PHASE_US > 0 && n >= kPhaseMinElements && group >= kEncPhaseMinGroup) {
+    const uint64_t us = bf16 ? SDP4_ENC_PHASE_US : SDP4_ENC_PHASE_US_F32;
+    const uint64_t pct = bf16 ? SDP4_ENC_READ_PCT : SDP4_ENC_READ_PCT_F32;
+    if (E == 32 && us > 0 && n >= kPhaseMinElements && group >= kEncPhaseMinGroup) {
         hipError_t err;
         const int khz = wall_clock_khz(err);
         if (err != hipSuccess)
@@ -30,8 +32,8 @@ int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, in
         // the period is set for the buffer of groups >= 128 and scales with
         // the buffer of the instantiation that runs
         const int cap = enc_phase_cap(group >= 128 ? 128 : 64);
-        period = khz > 0 ? (uint64_t)khz * SDP4_ENC_PHASE_US * cap / (1000 * enc_phase_cap(128)) : 0;
-        read_ticks = period * SDP4_ENC_READ_PCT / 100;
+        period = khz > 0 ? (uint64_t)khz * us * cap / (1000 * enc_phase_cap(128)) : 0;
+        read_ticks = period * pct / 100;
         // Both phases must last at least one clock tick, or a wave could wait
         // for a phase that never comes: otherwise stream.
         if (read_ticks == 0 || read_ticks >= period)

@@ -110,6 +110,12 @@
 #ifndef SDP4_ENC_READ_PCT
 #define SDP4_ENC_READ_PCT 92 // per cent of the period spent reading
 #endif
+#ifndef SDP4_ENC_PHASE_US_F32
+#define SDP4_ENC_PHASE_US_F32 90 // the same with float32 model weights (a tile reads a third more)
+#endif
+#ifndef SDP4_ENC_READ_PCT_F32
+#define SDP4_ENC_READ_PCT_F32 94
+#endif
 #ifndef SDP4_ENC_PHASE_DEPTH
 #define SDP4_ENC_PHASE_DEPTH 1 // tiles each phased encoder wave keeps loading ahead
 #endif
@@ -130,6 +136,7 @@ constexpr int kEncPhaseCap = SDP4_ENC_PHASE_CAP; // tiles buffered per wave by t
 constexpr int kEncPhaseCap64 = SDP4_ENC_PHASE_CAP64; // ... when its headers are those of groups of 64
 constexpr int kEncPhaseDepth = SDP4_ENC_PHASE_DEPTH;
 static_assert(SDP4_ENC_READ_PCT > 0 && SDP4_ENC_READ_PCT < 100, "the encoder's read phase is part of its period");
+static_assert(SDP4_ENC_READ_PCT_F32 > 0 && SDP4_ENC_READ_PCT_F32 < 100, "the encoder's read phase is part of its period");
 static_assert(SDP4_ENC_PHASE_CAP >= 1 && SDP4_ENC_PHASE_DEPTH >= 1, "phased encoder buffers");
 constexpr int kEncPhaseMinGroup = 64;       // smallest group the phased encoder buffers headers for
 // Tiles buffered per wave for a given smallest group: headers for groups of 64
