@@ -2,12 +2,13 @@
 configuration the benchmark times (paper_2410_15526_amd.pipeline.HotPath).
 
 The GPU runs one full step on the whole shard.  The oracle then recomputes
-sampled segments from regenerated inputs (the generators are addressable by
-element range), following the same chunk routing: an output segment of the
-final 4-bit reduction needs the matching segment of each of the Q 4-bit
-chunks, each of which needs the matching segment of each of the P 8-bit
-chunks.  Segments include the first and the last of every buffer (the
-ragged end of the last wave tile) and random ones in between.
+segments from regenerated inputs (the generators are addressable by element
+range), following the same chunk routing: an output segment of the final
+4-bit reduction needs the matching segment of each of the Q 4-bit chunks,
+each of which needs the matching segment of each of the P 8-bit chunks.
+Sampled segments include the first and the last of every buffer (the ragged
+end of the last wave tile) and random ones in between; on c1, c4 and c5
+every output element is compared.
 """
 import numpy as np
 import pytest
@@ -219,3 +220,76 @@ def test_shard_beyond_2_31_elements():
     big = [(1 << 31) - L, 1 << 31, (1 << 31) + 7 * L, w.n - L]
     check_qwd(hp, w, 0, big, L)
     check_gradient_path(hp, w, 0, big, segments(w.n // w.P // w.Q, L, 3, 7), L)
+
+
+def _pool():
+    import concurrent.futures as cf
+    import os
+    return cf.ThreadPoolExecutor(max(1, min(16, len(os.sched_getaffinity(0)))))
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["c4", "c5"])
+def test_full_shard_every_element(name):
+    """Every output of one step on the GPT-6.7B and GPT-13B shards against the
+    oracle: qWD codes, headers and decoded weights over the whole shard, K1
+    codes and scales of every element, K2 of every chunk, K3 of every output.
+    The oracle runs slice by slice in threads (its C calls release the
+    interpreter lock); slices follow the chunk routing of the step."""
+    w = synth.WORKLOADS[name]
+    seed = 0
+    hp = build(w, seed)
+    say(f"{name}: one step, every element")
+    hp.step()
+    torch().cuda.synchronize()
+    n, g, qg, P, Q, nb = w.n, w.group, w.qwd_group, w.P, w.Q, w.hadamard_block
+    M, m = n // P, n // P // Q
+    with _pool() as ex:
+        # qWD over the whole shard, in batches of B elements cut into slices of S
+        B, S = 1 << 27, 1 << 23
+        for a in range(0, n, B):
+            L = min(B, n - a)
+            new, prev = synth.new_weights(w, a, L, seed), synth.prev_weights(w, a, L, seed)
+            gc, gs, gm = host(hp.qcodes[a // 2:(a + L) // 2]), host(hp.qscale[a // qg:(a + L) // qg]), \
+                host(hp.qmin[a // qg:(a + L) // qg])
+            gw = host(hp.w_prev[a:a + L])
+
+            def qwd_slice(o, new=new, prev=prev, gc=gc, gs=gs, gm=gm, gw=gw, a=a, L=L):
+                k = min(S, L - o)
+                rc, rs, rm, pre = oracle.qwd_encode(new[o:o + k], prev[o:o + k], qg)
+                check_codes(gc[o // 2:(o + k) // 2], rc, pre, k, 4, signed=False, what=f"qwd@{a + o}")
+                check_headers(gs[o // qg:(o + k) // qg], rs, f"qscale@{a + o}")
+                check_headers(gm[o // qg:(o + k) // qg], rm, f"qmin@{a + o}")
+                want = oracle.qwd_decode(rc, rs, rm, prev[o:o + k], qg)
+                assert np.array_equal(gw[o:o + k].view(np.uint8), np.ascontiguousarray(want).view(np.uint8)), \
+                    f"decode@{a + o}"
+            list(ex.map(qwd_slice, range(0, L, S)))
+            del new, prev, gc, gs, gm, gw
+        say(f"{name}: qWD every element ok")
+        # the gradient chain, batch by batch of final outputs [a, a + L)
+        c8, s8, c4, s4, out = host(hp.c8), host(hp.s8), host(hp.c4), host(hp.s4), host(hp.out)
+        Lb = 1 << 21
+        for a in range(0, m, Lb):
+            L = min(Lb, m - a)
+
+            def k1(pq, a=a, L=L):
+                p, q = pq
+                x = p * M + q * m + a                          # input element of peer p's chunk q
+                rc, rs, pre = oracle.grad_quant(synth.gradient(w, x, L, seed), 8, nb, g)
+                check_codes(c8[x:x + L], rc, pre, L, 8, what=f"k1@{x}")
+                check_headers(s8[x // g:(x + L) // g], rs, f"k1 scale@{x}")
+                return rc, rs
+            r1 = list(ex.map(k1, [(p, q) for q in range(Q) for p in range(P)]))
+
+            def k2(q, a=a, L=L, r1=r1):
+                x = q * m + a
+                r = oracle.dequant_reduce([r1[q * P + p][0] for p in range(P)], [r1[q * P + p][1] for p in range(P)],
+                                          L, 8, g, 4, want_f32=False)
+                check_codes(c4[x // 2:(x + L) // 2], r["codes"], r["pre"], L, 4, what=f"k2@{x}")
+                check_headers(s4[x // g:(x + L) // g], r["scales"], f"k2 scale@{x}")
+                return r
+            r2 = list(ex.map(k2, range(Q)))
+            want = oracle.dequant_reduce([r["codes"] for r in r2], [r["scales"] for r in r2], L, 4, g, 0, nb,
+                                         1.0 / (P * Q))["f32"]
+            check_f32(out[a:a + L], want, f"k3@{a}")
+        say(f"{name}: gradient chain every element ok")
