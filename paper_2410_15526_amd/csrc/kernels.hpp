@@ -119,6 +119,9 @@
 #ifndef SDP4_ENC_PHASE_DEPTH
 #define SDP4_ENC_PHASE_DEPTH 1 // tiles each phased encoder wave keeps loading ahead
 #endif
+#ifndef SDP4_ENC_EARLY_LOAD_F32
+#define SDP4_ENC_EARLY_LOAD_F32 1 // phased encoder, float32 weights: a read phase's first tile loads the next first
+#endif
 #ifndef SDP4_ENC_HALF_T
 #define SDP4_ENC_HALF_T 1 // encoder: transpose its inputs through an LDS region of half a tile
 #endif
@@ -197,7 +200,12 @@ SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base 
 // other phase (0 < read_ticks < period, so both phases come round), and the
 // loop ends once the wave has no tile left and an empty buffer, so every
 // wave exits.  Results do not depend on the timing.
-template <int DEPTH, int WPB, class Tile, class Load, class Proc, class Flush>
+//
+// EARLY: the first tile of each read phase issues the next tile's loads
+// before its own compute (on a copy of its registers), while the memory
+// system would otherwise idle; later tiles compute first, keeping one load
+// in flight per wave.
+template <int DEPTH, int WPB, bool EARLY, class Tile, class Load, class Proc, class Flush>
 SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_t read_ticks, Load load, Proc proc,
                                Flush flush)
 {
@@ -211,6 +219,7 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
         if (t + k * stride < ntiles)
             load(t + k * stride, buf[k]);
     int nbuf = 0;
+    bool fresh = true; // no tile processed since the last flush or wait
     // Phase boundaries on the common grid of multiples of `period`, found by
     // one division here and then advanced by additions.
     uint64_t now = (uint64_t)wall_clock64();
@@ -226,19 +235,28 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
                     start += period;
                 const bool reading = now - start < read_ticks;
                 if (have && nbuf < cap && reading) {
-                    proc(t, buf[k], nbuf);
-                    ++nbuf;
-                    if (t + DEPTH * stride < ntiles)
+                    if (EARLY && fresh && t + DEPTH * stride < ntiles) {
+                        Tile cur = buf[k];
                         load(t + DEPTH * stride, buf[k]);
+                        proc(t, cur, nbuf);
+                    } else {
+                        proc(t, buf[k], nbuf);
+                        if (t + DEPTH * stride < ntiles)
+                            load(t + DEPTH * stride, buf[k]);
+                    }
+                    fresh = false;
+                    ++nbuf;
                     t += stride;
                     break;
                 } else if (nbuf > 0 && (!reading || !have)) {
                     flush(nbuf);
                     nbuf = 0;
+                    fresh = true;
                 } else if (!have) {
                     return; // no tile left and the buffer is empty
                 } else {
                     __builtin_amdgcn_s_sleep(1); // buffer full in a read phase, or empty in a write phase
+                    fresh = true;
                 }
             }
         }
@@ -457,7 +475,9 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
             }
             wave_lds_sync();
         };
-        phased_tile_loop<kEncPhaseDepth, WPB, Tile>(ntiles, CAP, period, read_ticks, load, proc, flush);
+        // early loads measured faster with float32 model weights only
+        constexpr bool EARLY = !BF16 && SDP4_ENC_EARLY_LOAD_F32;
+        phased_tile_loop<kEncPhaseDepth, WPB, EARLY, Tile>(ntiles, CAP, period, read_ticks, load, proc, flush);
     }
 }
 
