@@ -76,6 +76,11 @@ SDP4_DEV float xor_lane(float v)
 // lane falls back to the `old` operand.
 constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppRor8 = 0x128;
 
+// s_waitcnt immediate (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8) that waits for every outstanding vector-memory load and
+// for nothing else.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 template <int CTRL>
 SDP4_DEV uint32_t dpp_u32(uint32_t v)
 {

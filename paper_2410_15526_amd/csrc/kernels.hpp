@@ -122,6 +122,9 @@
 #ifndef SDP4_ENC_EARLY_LOAD_F32
 #define SDP4_ENC_EARLY_LOAD_F32 1 // phased encoder, float32 weights: a read phase's first tile loads the next first
 #endif
+#ifndef SDP4_ENC_EARLY_LOAD_BF16
+#define SDP4_ENC_EARLY_LOAD_BF16 0 // the same for bf16 weights
+#endif
 #ifndef SDP4_ENC_HALF_T
 #define SDP4_ENC_HALF_T 1 // encoder: transpose its inputs through an LDS region of half a tile
 #endif
@@ -237,6 +240,10 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
                 if (have && nbuf < cap && reading) {
                     if (EARLY && fresh && t + DEPTH * stride < ntiles) {
                         Tile cur = buf[k];
+                        // this tile's loads landed long ago: settle them before
+                        // the next ones go out, or the compiler's wait before the
+                        // first use of `cur` also waits for the new loads
+                        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
                         load(t + DEPTH * stride, buf[k]);
                         proc(t, cur, nbuf);
                     } else {
@@ -476,7 +483,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
             wave_lds_sync();
         };
         // early loads measured faster with float32 model weights only
-        constexpr bool EARLY = !BF16 && SDP4_ENC_EARLY_LOAD_F32;
+        constexpr bool EARLY = BF16 ? SDP4_ENC_EARLY_LOAD_BF16 : SDP4_ENC_EARLY_LOAD_F32;
         phased_tile_loop<kEncPhaseDepth, WPB, EARLY, Tile>(ntiles, CAP, period, read_ticks, load, proc, flush);
     }
 }
