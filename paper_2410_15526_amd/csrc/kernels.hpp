@@ -4,14 +4,18 @@
 // Every kernel is a persistent loop of wavefronts over wave tiles of 64*E
 // consecutive elements (see device.hpp for the lane layout).  Blocks hold
 // independent wavefronts, each with its own LDS staging region; no kernel
-// needs a block-wide barrier.  With a prefetch depth D >= 1 a wave issues
-// the global loads of its next D tiles before it processes the current one,
-// so HBM latency overlaps the LDS transposes, the arithmetic and the stores.
-// Everything a wave computes for a tile depends on that tile alone, so
-// results do not depend on the grid size or on the prefetching.
+// needs a block-wide barrier.  A wave keeps D >= 1 tile buffers and issues
+// a tile's global loads once it has processed the tile D places before it:
+// with the default D = 1 a wave's loads and its compute alternate, and the
+// other waves of the CU cover the load latency.  (With D >= 2 the compiler's
+// wait for one tile's loads also covers the later tiles' -- where a partial
+// tile's loads are guarded the number in flight depends on the path -- so
+// a deeper ring has not paid.)  Everything a wave computes for a tile
+// depends on that tile alone, so results do not depend on the grid size or
+// on D.
 //
 // The SDP4_* macros below are build-time tuning knobs; their defaults are
-// the measured best on MI355X: one tile prefetched, 32 elements per lane
+// the measured best on MI355X: one tile buffer per wave, 32 elements per lane
 // (16 for the 8-bit K1 with a transform and for the re-quantizing
 // dequantize-reduce of 8-bit messages, so that each lane loads one 16-byte
 // chunk per peer), and per kernel family a block shape -- one resident
@@ -26,7 +30,7 @@
 #include "launch.hpp"
 
 #ifndef SDP4_PIPE
-#define SDP4_PIPE 1 // tiles prefetched ahead of the one being processed
+#define SDP4_PIPE 1 // tile buffers per wave (a tile's loads follow the processing of the one D before)
 #endif
 #ifndef SDP4_PEER_LDS
 #define SDP4_PEER_LDS 1 // int8 peer chunks: coalesced loads + LDS transpose
@@ -153,9 +157,10 @@ constexpr int64_t kPhaseMinElements = 1 << 26; // smaller launches use the ordin
 
 // Persistent loop of one wavefront over its tiles t, t + S, t + 2S, ...
 // (S = waves in the grid, WPB waves per block).  DEPTH = 0 loads and
-// processes one tile at a time; DEPTH = D >= 1 keeps the loads of the next
-// D tiles in flight while a tile is processed (a ring of D register
-// buffers, indexed at compile time by unrolling).
+// processes one tile at a time; DEPTH = D >= 1 keeps a ring of D register
+// buffers (indexed at compile time by unrolling): a tile's loads go out
+// once the tile D places earlier is processed, so D - 1 later tiles are in
+// flight while one is processed.
 template <int DEPTH, int WPB, class Tile, class Load, class Proc>
 SDP4_DEV void tile_loop(int64_t ntiles, Load load, Proc proc)
 {
@@ -197,9 +202,9 @@ SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base 
 // wave-private LDS buffer of up to `cap` tiles, which they write out in the
 // rest of the period -- so the memory system sees long read-only and
 // write-only stretches instead of a mix.  proc(t, in, slot) computes tile t
-// into buffer slot `slot`; flush(k) writes slots 0..k-1.  DEPTH tiles are
-// prefetched (a ring of register buffers, indexed at compile time by
-// unrolling).  Every wait is a short sleep until the clock moves to the
+// into buffer slot `slot`; flush(k) writes slots 0..k-1.  DEPTH tile
+// buffers per wave, as in tile_loop (a ring of register buffers, indexed at
+// compile time by unrolling).  Every wait is a short sleep until the clock moves to the
 // other phase (0 < read_ticks < period, so both phases come round), and the
 // loop ends once the wave has no tile left and an empty buffer, so every
 // wave exits.  Results do not depend on the timing.
