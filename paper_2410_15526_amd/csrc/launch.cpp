@@ -60,6 +60,11 @@ int grid_for(const void *kernel, int64_t nwork_blocks, int per_cu_cap, int block
         }
         per_cu = it->second;
     }
+    // A launch whose work blocks all fit the device at full occupancy runs
+    // them all at once: it has no steady state for the per-CU cap to pace,
+    // and one round of tiles beats two.
+    if (nwork_blocks <= (int64_t)cus * per_cu)
+        return (int)(nwork_blocks > 0 ? nwork_blocks : 1);
     if (per_cu_cap > 0 && per_cu > per_cu_cap)
         per_cu = per_cu_cap;
     int64_t g = (int64_t)cus * per_cu;
