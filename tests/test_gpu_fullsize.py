@@ -244,6 +244,7 @@ def test_full_shard_every_element(name):
     torch().cuda.synchronize()
     n, g, qg, P, Q, nb = w.n, w.group, w.qwd_group, w.P, w.Q, w.hadamard_block
     M, m = n // P, n // P // Q
+    exempt = 0  # codes that differ at a near-tie (the parity bar's exemption), reported below
     with _pool() as ex:
         # qWD over the whole shard, in batches of B elements cut into slices of S
         B, S = 1 << 27, 1 << 23
@@ -257,13 +258,14 @@ def test_full_shard_every_element(name):
             def qwd_slice(o, new=new, prev=prev, gc=gc, gs=gs, gm=gm, gw=gw, a=a, L=L):
                 k = min(S, L - o)
                 rc, rs, rm, pre = oracle.qwd_encode(new[o:o + k], prev[o:o + k], qg)
-                check_codes(gc[o // 2:(o + k) // 2], rc, pre, k, 4, signed=False, what=f"qwd@{a + o}")
+                ties = check_codes(gc[o // 2:(o + k) // 2], rc, pre, k, 4, signed=False, what=f"qwd@{a + o}")
                 check_headers(gs[o // qg:(o + k) // qg], rs, f"qscale@{a + o}")
                 check_headers(gm[o // qg:(o + k) // qg], rm, f"qmin@{a + o}")
                 want = oracle.qwd_decode(rc, rs, rm, prev[o:o + k], qg)
                 assert np.array_equal(gw[o:o + k].view(np.uint8), np.ascontiguousarray(want).view(np.uint8)), \
                     f"decode@{a + o}"
-            list(ex.map(qwd_slice, range(0, L, S)))
+                return ties
+            exempt += sum(ex.map(qwd_slice, range(0, L, S)))
             del new, prev, gc, gs, gm, gw
         say(f"{name}: qWD every element ok")
         # the gradient chain, batch by batch of final outputs [a, a + L)
@@ -276,20 +278,26 @@ def test_full_shard_every_element(name):
                 p, q = pq
                 x = p * M + q * m + a                          # input element of peer p's chunk q
                 rc, rs, pre = oracle.grad_quant(synth.gradient(w, x, L, seed), 8, nb, g)
-                check_codes(c8[x:x + L], rc, pre, L, 8, what=f"k1@{x}")
+                ties = check_codes(c8[x:x + L], rc, pre, L, 8, what=f"k1@{x}")
                 check_headers(s8[x // g:(x + L) // g], rs, f"k1 scale@{x}")
-                return rc, rs
+                return rc, rs, ties
             r1 = list(ex.map(k1, [(p, q) for q in range(Q) for p in range(P)]))
+            exempt += sum(r[2] for r in r1)
 
             def k2(q, a=a, L=L, r1=r1):
                 x = q * m + a
                 r = oracle.dequant_reduce([r1[q * P + p][0] for p in range(P)], [r1[q * P + p][1] for p in range(P)],
                                           L, 8, g, 4, want_f32=False)
-                check_codes(c4[x // 2:(x + L) // 2], r["codes"], r["pre"], L, 4, what=f"k2@{x}")
+                r["ties"] = check_codes(c4[x // 2:(x + L) // 2], r["codes"], r["pre"], L, 4, what=f"k2@{x}")
                 check_headers(s4[x // g:(x + L) // g], r["scales"], f"k2 scale@{x}")
                 return r
             r2 = list(ex.map(k2, range(Q)))
+            exempt += sum(r["ties"] for r in r2)
             want = oracle.dequant_reduce([r["codes"] for r in r2], [r["scales"] for r in r2], L, 4, g, 0, nb,
                                          1.0 / (P * Q))["f32"]
             check_f32(out[a:a + L], want, f"k3@{a}")
         say(f"{name}: gradient chain every element ok")
+    # every code compared: n qWD codes, n K1 codes, n / P K2 codes
+    total = 2 * n + n // P
+    say(f"{name}: near-tie exemptions {exempt} of {total:,} codes")
+    assert exempt <= 1e-6 * total
