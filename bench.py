@@ -369,8 +369,8 @@ def main():
             del x, c, s, y
 
     # K3 standalone on N_in = N (the workload's element count) 4-bit inputs: Q chunks of N/Q
-    # elements reduced into N/Q fp32 outputs with the inverse Hadamard transform (in the chain K3 gets
-    # only N/P of them, too few launches' worth of tiles to reach the steady rate)
+    # elements reduced into N/Q fp32 outputs with the inverse Hadamard transform, its rate away from
+    # the ramp-up and the last partial round of a launch (in the chain it gets N/P inputs)
     standalone = {}
     if not args.no_standalone:
         hp = None  # the step's buffers are no longer needed
