@@ -109,7 +109,7 @@
 #endif
 
 #ifndef SDP4_ENC_PHASE_US
-#define SDP4_ENC_PHASE_US 68 // qWD encoder read/write period in microseconds (0: ordinary stream)
+#define SDP4_ENC_PHASE_US 66 // qWD encoder read/write period in microseconds (0: ordinary stream)
 #endif
 #ifndef SDP4_ENC_READ_PCT
 #define SDP4_ENC_READ_PCT 92 // per cent of the period spent reading
