@@ -177,7 +177,14 @@ class HotPath:
     # -- the unfused variant ("HS w/o fused") ----------------------------------
     def unfused_gradient_step(self, stream=None):
         """Same gradient path with the transform and the (de)quantization as
-        separate launches and float32 intermediates in HBM."""
+        separate launches and float32 intermediates in HBM.
+
+        The averaging factor ``out_scale`` rides on the second-level
+        dequantization of each chunk (no extra pass).  For the power-of-two
+        1/(P*Q) of every workload here, scaling commutes exactly with the
+        float32 sum and the transform that follow (barring subnormals), so
+        the result is the fused path's up to the rounding of the separate
+        products and sums."""
         import torch
         if self._unfused is None:
             e = lambda k, dt: torch.empty(k, dtype=dt, device=self.grad.device)
@@ -196,7 +203,7 @@ class HotPath:
         sdp4.sdp4_grad_quant(u["r"], 4, 0, g, self.c4, self.s4, stream=stream)
         c, s = self.inter_chunks()
         for q in range(Q):
-            sdp4.sdp4_dequant_reduce([c[q]], [s[q]], m, 4, g, 0, 0, 1.0, None, None, u["d2"][q * m:(q + 1) * m],
-                                     stream=stream)
+            sdp4.sdp4_dequant_reduce([c[q]], [s[q]], m, 4, g, 0, 0, self.out_scale, None, None,
+                                     u["d2"][q * m:(q + 1) * m], stream=stream)
         sdp4.sdp4_reduce_f32([u["d2"][q * m:(q + 1) * m] for q in range(Q)], u["r2"], stream=stream)
         sdp4.sdp4_hadamard(u["r2"], self.out, self.block, stream=stream)

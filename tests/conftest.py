@@ -16,6 +16,8 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an AMD Instinct GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running (full-size workloads)")
+    config.addinivalue_line("markers", "cpu_only: hands the library made-up device addresses; "
+                                       "skipped where a GPU is visible")
 
 
 def pytest_collection_modifyitems(config, items):
@@ -28,6 +30,10 @@ def pytest_collection_modifyitems(config, items):
     except Exception:
         pass
     if have_gpu:
+        skip_cpu = pytest.mark.skip(reason="made-up device addresses are tested only without a GPU")
+        for it in items:
+            if "cpu_only" in it.keywords:
+                it.add_marker(skip_cpu)
         return
     skip = pytest.mark.skip(reason="no GPU on this host")
     for it in items:

@@ -1,7 +1,11 @@
 """The C ABI library on a host without a GPU: it loads, exports every entry
 point the public header declares, and rejects invalid arguments on the
 host with the documented status before anything reaches the device (these
-calls never launch a kernel)."""
+calls never launch a kernel).
+
+Tests that hand the library made-up device addresses carry the ``cpu_only``
+marker and are skipped where a GPU is visible: there a lapse in the
+library's checks would launch a kernel on unmapped memory."""
 import ctypes as C
 import math
 import os
@@ -54,6 +58,7 @@ def gq(x=A, n=4096, bits=8, block=256, group=128, codes=B, scale=CC):
     return sdp4.lib().sdp4_grad_quant(x, n, bits, block, group, codes, scale, None)
 
 
+@pytest.mark.cpu_only
 @pytest.mark.parametrize("kw,want", [
     (dict(bits=3), EINVAL), (dict(bits=2), EINVAL), (dict(group=48), EINVAL), (dict(group=16), EINVAL),
     (dict(group=8192), EINVAL), (dict(block=3), EINVAL), (dict(block=2048), EINVAL), (dict(block=1), EINVAL),
@@ -77,6 +82,7 @@ def dec(codes=A, scale=B, minv=B + 4096, n=4096, group=128, w=CC, dt=0):
     return sdp4.lib().sdp4_qwd_decode(codes, scale, minv, n, group, w, dt, None)
 
 
+@pytest.mark.cpu_only
 @pytest.mark.parametrize("kw,want", [
     (dict(dt=2), EINVAL), (dict(dt=-1), EINVAL), (dict(group=100), EINVAL), (dict(n=4000), EALIGN),
     (dict(w_new=None), EINVAL), (dict(minv=None), EINVAL), (dict(w_prev=B + 2), EALIGN),
@@ -88,6 +94,7 @@ def test_qwd_encode_validation(kw, want):
     assert enc(**kw) == want
 
 
+@pytest.mark.cpu_only
 @pytest.mark.parametrize("kw,want", [
     (dict(dt=7), EINVAL), (dict(group=64 + 32), EINVAL), (dict(n=4096 + 64), EALIGN), (dict(w=None), EINVAL),
     (dict(w=CC + 8), EALIGN), (dict(codes=A + 8), EALIGN), (dict(w=A + 512), EINVAL),
@@ -105,6 +112,7 @@ def dec_sym(codes=A, scale=B, n=4096, group=128, w=CC, dt=0):
     return sdp4.lib().sdp4_qwd_decode_sym(codes, scale, n, group, w, dt, None)
 
 
+@pytest.mark.cpu_only
 @pytest.mark.parametrize("kw,want", [
     (dict(dt=2), EINVAL), (dict(group=100), EINVAL), (dict(group=8192), EINVAL), (dict(n=4000), EALIGN),
     (dict(n=-128), EINVAL), (dict(w_new=None), EINVAL), (dict(w_prev=None), EINVAL), (dict(codes=None), EINVAL),
@@ -116,6 +124,7 @@ def test_qwd_encode_sym_validation(kw, want):
     assert enc_sym(**kw) == want
 
 
+@pytest.mark.cpu_only
 @pytest.mark.parametrize("kw,want", [
     (dict(dt=7), EINVAL), (dict(group=96), EINVAL), (dict(n=4096 + 64), EALIGN), (dict(w=None), EINVAL),
     (dict(codes=None), EINVAL), (dict(scale=None), EINVAL), (dict(w=CC + 8), EALIGN),
@@ -140,6 +149,7 @@ def dr(P=4, codes=None, scales=None, n=4096, bits_in=8, group=128, bits_out=4, b
                                           of, None)
 
 
+@pytest.mark.cpu_only
 @pytest.mark.parametrize("kw,want", [
     (dict(P=0), ERANGE), (dict(P=17, codes=[A] * 17, scales=[B] * 17), ERANGE), (dict(P=-3), ERANGE),
     (dict(bits_in=2), EINVAL), (dict(bits_out=2), EINVAL), (dict(bits_out=4, block=64), EINVAL),
@@ -159,6 +169,7 @@ def test_dequant_reduce_validation(kw, want):
     assert dr(**kw) == want
 
 
+@pytest.mark.cpu_only
 def test_hadamard_reduce_copy_validation():
     L = sdp4.lib()
     assert L.sdp4_hadamard(A, B, 4096, 0, None) == EINVAL
@@ -179,6 +190,7 @@ def test_hadamard_reduce_copy_validation():
     assert L.sdp4_copy_f32(A, B, 0, None) == OK
 
 
+@pytest.mark.cpu_only
 def test_element_counts_beyond_the_limit_are_rejected():
     big = (1 << 48) + 4096
     L = sdp4.lib()
@@ -200,6 +212,7 @@ def test_binding_refuses_host_tensors():
         sdp4.sdp4_grad_quant(x, 8, 256, 128, x, x)
 
 
+@pytest.mark.cpu_only
 def test_stochastic_rounding_entry_points_validation():
     L = sdp4.lib()
     args = lambda **k: dict(dict(x=A, n=4096, bits=8, block=256, group=128, seed=1, offset=0, codes=B, scale=CC), **k)
@@ -224,6 +237,7 @@ def test_stochastic_rounding_entry_points_validation():
     assert dr(n=0) == OK
 
 
+@pytest.mark.cpu_only
 def test_header_is_c99_and_a_c_program_links(tmp_path):
     """The boundary is a C ABI: the header compiles as strict C99 and a C
     program links against the library and gets the documented statuses."""
@@ -236,7 +250,8 @@ def test_header_is_c99_and_a_c_program_links(tmp_path):
            os.path.join(ROOT, "tests", "abi_c_client.c"), "-L", libdir, "-lsdp4", f"-Wl,-rpath,{libdir}",
            "-o", str(exe)]
     subprocess.run(cmd, check=True, capture_output=True)
-    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    env = dict(os.environ, HIP_VISIBLE_DEVICES="", ROCR_VISIBLE_DEVICES="")   # no device to launch on
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True, env=env).stdout.split("\n")
     assert out[:10] == ["1", "2", "0", "3", "1", "2", "2048", "32", "peer count out of range", "0"]
 
 

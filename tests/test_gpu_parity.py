@@ -512,6 +512,48 @@ def test_unfused_chain_matches_oracle():
     check_f32(host(out), want)
 
 
+def test_hotpath_unfused_step_matches_fused_and_its_oracle():
+    """HotPath.unfused_gradient_step on a scaled GPT-1.3B shard (P = 8, Q = 4,
+    block 256): its output is the oracle's unfused composition bit for bit,
+    averaging included, and within the float bar of the fused step."""
+    from paper_2410_15526_amd.pipeline import HotPath
+    w = synth.scaled(synth.WORKLOADS["c3"], 1 << 22)
+    n, g, blk, P, Q = w.n, w.group, w.hadamard_block, w.P, w.Q
+    M, m, osc = n // P, n // (P * Q), 1.0 / (P * Q)
+    say(f"HotPath unfused vs fused n={n} P={P} Q={Q} block={blk}")
+    grad = synth.gradient(w, 0, n, 0)
+    hp = HotPath(n, g, blk, P, Q, w.qwd_group, w.prev_dtype)
+    hp.grad.copy_(torch().from_numpy(grad))
+    hp.grad_quant()
+    hp.reduce_intra()
+    hp.reduce_inter()
+    sync()
+    fused = host(hp.out).copy()
+    hp.out.fill_(-1.0)
+    hp.unfused_gradient_step()
+    sync()
+    unfused = host(hp.out).copy()
+
+    c8, s8, _ = oracle.grad_quant(grad, 8, blk, g)
+    k2 = oracle.dequant_reduce([c8[p * M:(p + 1) * M] for p in range(P)],
+                               [s8[p * M // g:(p + 1) * M // g] for p in range(P)], M, 8, g, 4)
+    c4, s4 = k2["codes"], k2["scales"]
+    want_fused = oracle.dequant_reduce([c4[q * m // 2:(q + 1) * m // 2] for q in range(Q)],
+                                       [s4[q * m // g:(q + 1) * m // g] for q in range(Q)], m, 4, g, 0, blk,
+                                       osc)["f32"]
+    hc8, hs8, _ = oracle.grad_quant(oracle.hadamard(grad, blk), 8, 0, g)
+    d = [oracle.dequant_reduce([hc8[p * M:(p + 1) * M]], [hs8[p * M // g:(p + 1) * M // g]], M, 8, g, 0)["f32"]
+         for p in range(P)]
+    uc4, us4, _ = oracle.grad_quant(oracle.reduce_f32(d), 4, 0, g)
+    d2 = [oracle.dequant_reduce([uc4[q * m // 2:(q + 1) * m // 2]], [us4[q * m // g:(q + 1) * m // g]], m, 4, g,
+                                0, 0, osc)["f32"] for q in range(Q)]
+    want_unfused = oracle.hadamard(oracle.reduce_f32(d2), blk)
+
+    check_f32(fused, want_fused, "fused step")
+    check_f32(unfused, want_unfused, "unfused step")
+    check_f32(unfused, fused, "unfused vs fused", exact=False)
+
+
 # ----------------------------------------------------------------------------
 # determinism, empty inputs, binding errors
 # ----------------------------------------------------------------------------

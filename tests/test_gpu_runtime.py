@@ -16,8 +16,8 @@ from tests._gpu import fill, host, say, torch
 pytestmark = pytest.mark.gpu
 
 
-def small_path(seed=0):
-    w = synth.WORKLOADS["c1"]
+def make_path(name="c1", n=None, seed=0):
+    w = synth.WORKLOADS[name] if n is None else synth.scaled(synth.WORKLOADS[name], n)
     hp = HotPath(w.n, w.group, w.hadamard_block, w.P, w.Q, w.qwd_group, w.prev_dtype)
     fill(hp.w_prev, lambda s, k: synth.prev_weights(w, s, k, seed), w.n)
     fill(hp.w_new, lambda s, k: synth.new_weights(w, s, k, seed), w.n)
@@ -30,10 +30,15 @@ def outputs(hp):
     return [host(t).copy() for t in (hp.qcodes, hp.qscale, hp.qmin, hp.w_prev, hp.c8, hp.s8, hp.c4, hp.s4, hp.out)]
 
 
-def test_step_replayed_from_a_hip_graph():
+@pytest.mark.parametrize("name,n", [("c1", None), ("c5", 1 << 26)])
+def test_step_replayed_from_a_hip_graph(name, n):
+    """c1: the tiny shard (streaming kernels).  c5 scaled to 2^26 elements:
+    bfloat16 model weights and groups of 128, so the encoder runs in its
+    clock-phased mode (launches of at least 2^26 elements), whose period the
+    host computes from the device's wall-clock rate at capture time."""
     t = torch()
-    say("graph capture of one step")
-    hp = small_path()
+    say(f"graph capture of one step: {name} n={n}")
+    hp = make_path(name, n)
     prev0 = hp.w_prev.clone()
     hp.step()                                   # eager step (also warms the launch caches)
     t.cuda.synchronize()
