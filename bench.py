@@ -14,8 +14,13 @@ kernel the line also carries algorithmic HBM bytes / launch time against the
 (``vs_copy``); ``roofline`` is the peak figure for the kernel that takes the
 largest share of the step.  ``cpu_baseline`` is the plain CPU oracle timed
 on a bounded sample of the same workload on this host (single thread);
-``cpu_baseline_all_cores`` the same oracle on the same sample split into one
-slice per available core (up to 16), each in its own thread.
+``cpu_baseline_all_cores`` the same oracle over the whole workload split into
+one slice per available core (up to 16), each in its own thread.
+``ceilings`` holds what HBM gives plain streams at the step's array size
+(read-only, write-only and copy yardsticks of the library, the runtime's own
+copy and fill); each kernel's ``vs_rw_additive`` compares it with a kernel
+that moved its reads at the read-only rate and its writes at the write-only
+rate, one after the other.
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 20] [--workload c5]
 """
@@ -144,29 +149,63 @@ def cpu_baseline(w, sample_log2: int, seed: int):
                       f"plain C oracle"}
 
 
-def cpu_baseline_all_cores(w, sample_log2: int, seed: int, max_threads: int = 16):
-    """The same oracle on the same sample, split into one contiguous slice per
-    available core (at most max_threads), each slice a full step of its own in
-    its own thread (the oracle's C calls release the interpreter lock).
-    Groups and blocks are independent, so every slice computes exactly what
-    the single-threaded run computes for those elements."""
+def cpu_baseline_all_cores(w, n_total: int, seed: int, max_threads: int = 16):
+    """The same oracle on elements [0, n_total) of the workload, split into one
+    contiguous slice per available core (at most max_threads), each slice a
+    full step of its own in its own thread (the oracle's C calls release the
+    interpreter lock).  Groups and blocks are independent, so every slice
+    computes exactly what a single-threaded run computes for those elements.
+    The inputs are generated before the clock starts."""
     import concurrent.futures as cf
     import math
-    n = 1 << sample_log2
     T = max(1, min(len(os.sched_getaffinity(0)), max_threads))
     unit = w.P * w.Q * math.lcm(w.group, w.hadamard_block or 1, w.qwd_group)
-    per = n // T // unit * unit
+    per = n_total // T // unit * unit
     if per == 0:
-        T, per = 1, n
+        T, per = 1, n_total // unit * unit
     slices = [_oracle_inputs(w, i * per, per, seed) for i in range(T)]
     with cf.ThreadPoolExecutor(T) as ex:
         t0 = time.perf_counter()
         list(ex.map(lambda a: _oracle_step(w, *a), slices))
         dt = time.perf_counter() - t0
+    whole = "the whole workload" if T * per == w.n else f"elements [0, {T * per}) of the same workload"
     return {"value": round(_step_fp32_bytes(w, per) * T / dt / 1e9, 4), "unit": "GB/s", "cores": T,
             "kind": "oracle", "seconds": round(dt, 3), "host_cpu": host_cpu(),
-            "sample": f"elements [0, {T * per}) of the same workload in {T} slices of {per}, {_step_desc(w)} "
-                      f"per slice, one thread per slice, plain C oracle"}
+            "sample": f"{whole} in {T} slices of {per}, {_step_desc(w)} per slice, one thread per slice, "
+                      f"plain C oracle"}
+
+
+def ceilings(n: int, timed):
+    """What HBM gives plain streams at the step's own array size (n float32
+    elements, 4n bytes each way): the library's read-only, write-only and copy
+    yardsticks, and the runtime's own device-to-device copy and fill."""
+    import torch
+    from paper_2410_15526_amd import sdp4
+    x = torch.empty(n, device="cuda")
+    y = torch.empty(n, device="cuda")
+    sdp4.sdp4_fill_f32(x, 1.0)
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    gb = lambda nbytes, ms: round(nbytes / (ms * 1e-3) / 1e9, 1)
+    out = {"array_bytes": 4 * n}
+    out["read_GBps"] = gb(4 * n, timed(lambda: sdp4.sdp4_read_f32(x, sink), reps=5))
+    out["write_GBps"] = gb(4 * n, timed(lambda: sdp4.sdp4_fill_f32(y, 0.0), reps=5))
+    out["copy_GBps"] = gb(8 * n, timed(lambda: sdp4.sdp4_copy_f32(x, y), reps=5))
+    out["runtime_copy_GBps"] = gb(8 * n, timed(lambda: y.copy_(x), reps=5))
+    out["runtime_fill_GBps"] = gb(4 * n, timed(lambda: y.fill_(0.5), reps=5))
+    for k in list(out):
+        if k.endswith("_GBps"):
+            out[k.replace("_GBps", "_frac")] = round(out[k] / HBM_PEAK_GBPS, 4)
+    del x, y, sink
+    torch.cuda.empty_cache()
+    return out
+
+
+def rw_additive_GBps(read_bytes: int, write_bytes: int, c: dict) -> float:
+    """Rate of a kernel that moved its reads at the read-only ceiling and
+    its writes at the write-only ceiling, one after the other (no penalty
+    for mixing the two: an upper bound)."""
+    t = read_bytes / (c["read_GBps"] * 1e9) + write_bytes / (c["write_GBps"] * 1e9)
+    return (read_bytes + write_bytes) / t / 1e9
 
 
 def main():
@@ -183,6 +222,7 @@ def main():
     ap.add_argument("--no-table5", action="store_true")
     ap.add_argument("--no-standalone", action="store_true")
     ap.add_argument("--no-group-sweep", action="store_true")
+    ap.add_argument("--no-ceilings", action="store_true")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -297,6 +337,18 @@ def main():
         torch.cuda.synchronize()
         return round(a.elapsed_time(b) / reps, 4)
 
+    # read-only / write-only / copy ceilings at the step's array size, and each kernel against the
+    # bound its own mix of reads and writes would have at those rates
+    ceil = None
+    if not args.no_ceilings:
+        ceil = ceilings(w.n, timed)
+        for name, k in kernels.items():
+            ki = info[name]
+            bound = rw_additive_GBps(ki.read_bytes, ki.alg_bytes - ki.read_bytes, ceil)
+            k["read_share"] = round(ki.read_bytes / ki.alg_bytes, 4)
+            k["rw_additive_GBps"] = round(bound, 1)
+            k["vs_rw_additive"] = round(k["alg_GBps"] / bound, 4)
+
     variants = {}
     if not args.no_variants:
         for v in ("tlq_hs", "tlq", "ulq", "tlq_hs_sr"):
@@ -388,6 +440,9 @@ def main():
         gbps = alg / (ms * 1e-3) / 1e9
         standalone["reduce_inter"] = {"n_in": Q * m, "ms": ms, "alg_bytes": alg, "alg_GBps": round(gbps, 1),
                                       "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+        if ceil:
+            rd = Q * (m // 2 + 4 * (m // g))
+            standalone["reduce_inter"]["vs_rw_additive"] = round(gbps / rw_additive_GBps(rd, alg - rd, ceil), 4)
         del c4, s4, out, cl, sl
 
     traffic = traffic_for(dom, args.workload)
@@ -422,13 +477,15 @@ def main():
         line["table5_sweep"] = table5
     if standalone:
         line["standalone"] = standalone
+    if ceil:
+        line["ceilings"] = ceil
     if group_sweep:
         line["group_sweep"] = group_sweep
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample ...")
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_log2, args.seed)
-        log("timing the CPU oracle on all cores ...")
-        line["cpu_baseline_all_cores"] = cpu_baseline_all_cores(w, args.cpu_sample_log2, args.seed)
+        log("timing the CPU oracle on all cores over the whole workload ...")
+        line["cpu_baseline_all_cores"] = cpu_baseline_all_cores(w, w.n, args.seed)
     print(json.dumps(line), flush=True)
 
 

@@ -273,6 +273,25 @@ int sdp4_reduce_f32(int P, const float *const *xs, float *y, int64_t n, void *st
  */
 int sdp4_copy_f32(const float *x, float *y, int64_t n, void *stream);
 
+/*
+ * Read-only stream over x[0..n) (a bandwidth yardstick: the rate HBM gives
+ * pure reads).  XOR-accumulates the bit patterns of x[i] into sink[i % 4]:
+ *   x    [n] device, 16-byte aligned
+ *   sink [4] device uint32, 4-byte aligned, must not overlap x; the caller
+ *        clears it first (the call only XORs into it)
+ * Errors: EINVAL (null pointer, n < 0 or beyond the limit, overlap), EALIGN,
+ * EHIP.
+ */
+int sdp4_read_f32(const float *x, int64_t n, uint32_t *sink, void *stream);
+
+/*
+ * Write-only stream y[i] = value for i in [0, n) (a bandwidth yardstick: the
+ * rate HBM gives pure writes).
+ *   y [n] device, 16-byte aligned
+ * Errors: EINVAL, EALIGN, EHIP.
+ */
+int sdp4_fill_f32(float *y, int64_t n, float value, void *stream);
+
 /* Pure helpers (no device work). */
 int64_t sdp4_codes_bytes(int64_t n, int bits);  /* n * bits / 8, or -1 if bits not 4 or 8 */
 int64_t sdp4_num_groups(int64_t n, int group); /* n / group, or -1 if not a valid group */

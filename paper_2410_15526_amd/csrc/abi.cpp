@@ -322,6 +322,34 @@ int sdp4_copy_f32(const float *x, float *y, int64_t n, void *stream)
     return sdp4::launch_copy_f32(x, y, n, as_stream(stream));
 }
 
+int sdp4_read_f32(const float *x, int64_t n, uint32_t *sink, void *stream)
+{
+    if (!valid_n(n))
+        return SDP4_EINVAL;
+    if (n == 0)
+        return SDP4_OK;
+    if (!x || !sink)
+        return SDP4_EINVAL;
+    if (!aligned(x, 16) || !aligned(sink, 4))
+        return SDP4_EALIGN;
+    if (overlap(x, 4 * n, sink, 16))
+        return SDP4_EINVAL;
+    return sdp4::launch_read_f32(x, n, sink, as_stream(stream));
+}
+
+int sdp4_fill_f32(float *y, int64_t n, float value, void *stream)
+{
+    if (!valid_n(n))
+        return SDP4_EINVAL;
+    if (n == 0)
+        return SDP4_OK;
+    if (!y)
+        return SDP4_EINVAL;
+    if (!aligned(y, 16))
+        return SDP4_EALIGN;
+    return sdp4::launch_fill_f32(y, n, value, as_stream(stream));
+}
+
 int64_t sdp4_codes_bytes(int64_t n, int bits)
 {
     if (!valid_n(n) || !valid_bits(bits))

@@ -14,11 +14,11 @@ struct GradQuantSR {
         if (use_wide_lanes(group, 32)) {   // 64 elements per lane: the default shape's register budget
             constexpr int WPB = kWavesPerBlock;
             auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth, WPB, true> : k_grad_quant<4, 64, NB, kDepth, WPB, true>;
-            return launch<WPB>(k, wave_blocks<WPB>(n, 64), kCap, s, x, n, group, cn, codes, scale, seed, offset);
+            return launch<WPB>(k, wave_blocks<WPB>(n, 64), kK1SrCap, s, x, n, group, cn, codes, scale, seed, offset);
         }
         constexpr int WPB = kK1Waves32;
         auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth, WPB, true> : k_grad_quant<4, 32, NB, kDepth, WPB, true>;
-        return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, seed, offset);
+        return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1SrCap, s, x, n, group, cn, codes, scale, seed, offset);
     }
 };
 

@@ -18,12 +18,18 @@
 // the measured best on MI355X: one tile buffer per wave, 32 elements per lane
 // (16 for the 8-bit K1 with a transform and for the re-quantizing
 // dequantize-reduce of 8-bit messages, so that each lane loads one 16-byte
-// chunk per peer), and per kernel family a block shape -- one resident
-// block of four waves per CU for the qWD encoder and decoder, one block of
-// eight waves for K1 (four without a transform) and for the 8-bit K2, two
-// blocks of four waves for the rest.  (How many bytes a CU keeps in flight,
-// and how far compute spreads its requests out, moves the mixed read/write
-// bandwidth of HBM by several per cent.)
+// chunk per peer), and per kernel family a block shape and a grid mode.
+// Most kernels launch one block per work block, which the hardware
+// dispatches in address order, so the chip's accesses sweep memory front to
+// back (HBM serves that faster than the scattered fronts of a persistent
+// grid), with a cap on resident blocks per CU where that measured faster:
+// decode 2 blocks of four waves, K1 3 blocks of eight (of four without a
+// transform), K2 on 8-bit messages 2 blocks of eight, K3 and the rest 4
+// blocks of four.  The clock-phased qWD encoder (one block of four waves
+// per CU) and K1 with stochastic rounding (one block of eight) keep
+// persistent grids.  (How many bytes a CU keeps in flight, and how far
+// compute spreads its requests out, moves the mixed read/write bandwidth of
+// HBM by several per cent.)
 #pragma once
 
 #include "device.hpp"
@@ -55,8 +61,12 @@
 // lane; groups up to 1024).
 #define SDP4_E_RQ8 16
 #endif
+// Block caps: n > 0 runs a persistent grid of at most n resident blocks per
+// compute unit (0: as many as fit); -k (k < 64) one block per work block,
+// dispatched in address order, at most k resident per compute unit;
+// -64 the same with residency left to occupancy (launch.hpp, kFullGrid).
 #ifndef SDP4_BLOCKS_PER_CU
-#define SDP4_BLOCKS_PER_CU 2 // resident blocks per compute unit (0: as many as fit)
+#define SDP4_BLOCKS_PER_CU -4 // block cap of the kernels without one of their own below
 #endif
 // Block shape (waves per block, resident blocks per compute unit) of the qWD
 // encoder and of K1; every other kernel uses SDP4_WAVES_PER_BLOCK (device.hpp)
@@ -76,8 +86,11 @@
 #ifndef SDP4_K1_WAVES_PLAIN
 #define SDP4_K1_WAVES_PLAIN 4 // K1 without a transform (32 elements per lane)
 #endif
+#ifndef SDP4_K1_SR_BPC
+#define SDP4_K1_SR_BPC 1 // K1 with stochastic rounding: one persistent block per compute unit
+#endif
 #ifndef SDP4_K1_BPC
-#define SDP4_K1_BPC 1
+#define SDP4_K1_BPC -3
 #endif
 
 // Block shapes of the qWD decoder, of the dequantize-reduce with
@@ -87,25 +100,25 @@
 #define SDP4_DEC_WAVES 4
 #endif
 #ifndef SDP4_DEC_BPC
-#define SDP4_DEC_BPC 1
+#define SDP4_DEC_BPC -2
 #endif
 #ifndef SDP4_RQ_WAVES
 #define SDP4_RQ_WAVES 4
 #endif
 #ifndef SDP4_RQ_BPC
-#define SDP4_RQ_BPC 2
+#define SDP4_RQ_BPC -4
 #endif
 #ifndef SDP4_RQ8_WAVES // ... of 8-bit messages with 16 elements per lane
 #define SDP4_RQ8_WAVES 8
 #endif
 #ifndef SDP4_RQ8_BPC
-#define SDP4_RQ8_BPC 1
+#define SDP4_RQ8_BPC -2
 #endif
 #ifndef SDP4_RF_WAVES
 #define SDP4_RF_WAVES 4
 #endif
 #ifndef SDP4_RF_BPC
-#define SDP4_RF_BPC 2
+#define SDP4_RF_BPC -4
 #endif
 
 #ifndef SDP4_ENC_PHASE_US
@@ -817,6 +830,7 @@ int64_t wave_blocks(int64_t n, int E)
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
 constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC;
 constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
+constexpr int kK1SrCap = SDP4_K1_SR_BPC;
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;

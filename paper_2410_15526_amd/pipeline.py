@@ -27,6 +27,7 @@ class KernelInfo:
     name: str
     alg_bytes: int        # bytes the method must move per launch (reads + writes)
     fp32_in_bytes: int    # 4 x input elements (the "fp32 input processed" yardstick)
+    read_bytes: int = 0   # the reads among alg_bytes (the rest are writes)
 
 
 class HotPath:
@@ -167,11 +168,14 @@ class HotPath:
         n, g, qg, P, Q, M, m = self.n, self.group, self.qwd_group, self.P, self.Q, self.M, self.m
         esz = 2 if self.prev_dtype == "bf16" else 4
         return {
-            "qwd_encode": KernelInfo("qwd_encode", 4 * n + esz * n + n // 2 + 8 * (n // qg), 4 * n),
-            "qwd_decode": KernelInfo("qwd_decode", n // 2 + 8 * (n // qg) + 2 * esz * n, 4 * n),
-            "grad_quant": KernelInfo("grad_quant", 4 * n + n + 4 * (n // g), 4 * n),
-            "reduce_intra": KernelInfo("reduce_intra", P * (M + 4 * (M // g)) + M // 2 + 4 * (M // g), 4 * P * M),
-            "reduce_inter": KernelInfo("reduce_inter", Q * (m // 2 + 4 * (m // g)) + 4 * m, 4 * Q * m),
+            "qwd_encode": KernelInfo("qwd_encode", 4 * n + esz * n + n // 2 + 8 * (n // qg), 4 * n, 4 * n + esz * n),
+            "qwd_decode": KernelInfo("qwd_decode", n // 2 + 8 * (n // qg) + 2 * esz * n, 4 * n,
+                                     n // 2 + 8 * (n // qg) + esz * n),
+            "grad_quant": KernelInfo("grad_quant", 4 * n + n + 4 * (n // g), 4 * n, 4 * n),
+            "reduce_intra": KernelInfo("reduce_intra", P * (M + 4 * (M // g)) + M // 2 + 4 * (M // g), 4 * P * M,
+                                       P * (M + 4 * (M // g))),
+            "reduce_inter": KernelInfo("reduce_inter", Q * (m // 2 + 4 * (m // g)) + 4 * m, 4 * Q * m,
+                                       Q * (m // 2 + 4 * (m // g))),
         }
 
     # -- the unfused variant ("HS w/o fused") ----------------------------------

@@ -54,6 +54,8 @@ def lib() -> C.CDLL:
                 "sdp4_hadamard": (i32, [vp, vp, i64, i32, vp]),
                 "sdp4_reduce_f32": (i32, [i32, vp, vp, i64, vp]),
                 "sdp4_copy_f32": (i32, [vp, vp, i64, vp]),
+                "sdp4_read_f32": (i32, [vp, i64, vp, vp]),
+                "sdp4_fill_f32": (i32, [vp, i64, f32, vp]),
                 "sdp4_codes_bytes": (i64, [i64, i32]),
                 "sdp4_num_groups": (i64, [i64, i32]),
                 "sdp4_status_string": (C.c_char_p, [i32]),
@@ -233,6 +235,20 @@ def sdp4_copy_f32(x, y, n=None, stream=None):
     n = x.numel() if n is None else n
     _need(x, 4 * n, "x"); _need(y, 4 * n, "y")
     _ck("sdp4_copy_f32", lib().sdp4_copy_f32(_ptr(x), _ptr(y), n, _stream(stream)))
+
+
+def sdp4_read_f32(x, sink, n=None, stream=None):
+    """Read-only stream over x; XORs the bit patterns of x[i] into sink[i % 4]
+    (sink: 4 int32 or uint32 words on the device, cleared by the caller)."""
+    n = x.numel() if n is None else n
+    _need(x, 4 * n, "x"); _need(sink, 16, "sink")
+    _ck("sdp4_read_f32", lib().sdp4_read_f32(_ptr(x), n, _ptr(sink), _stream(stream)))
+
+
+def sdp4_fill_f32(y, value, n=None, stream=None):
+    n = y.numel() if n is None else n
+    _need(y, 4 * n, "y")
+    _ck("sdp4_fill_f32", lib().sdp4_fill_f32(_ptr(y), n, float(value), _stream(stream)))
 
 
 def sdp4_codes_bytes(n, bits):

@@ -191,6 +191,22 @@ def test_hadamard_reduce_copy_validation():
 
 
 @pytest.mark.cpu_only
+def test_yardstick_validation():
+    L = sdp4.lib()
+    assert L.sdp4_read_f32(None, 4096, B, None) == EINVAL
+    assert L.sdp4_read_f32(A, 4096, None, None) == EINVAL
+    assert L.sdp4_read_f32(A + 4, 4096, B, None) == EALIGN
+    assert L.sdp4_read_f32(A, 4096, B + 2, None) == EALIGN
+    assert L.sdp4_read_f32(A, 4096, A + 64, None) == EINVAL                   # sink inside x
+    assert L.sdp4_read_f32(A, -1, B, None) == EINVAL
+    assert L.sdp4_read_f32(A, 0, B, None) == OK
+    assert L.sdp4_fill_f32(None, 4096, 1.0, None) == EINVAL
+    assert L.sdp4_fill_f32(A + 8, 4096, 1.0, None) == EALIGN
+    assert L.sdp4_fill_f32(A, -5, 1.0, None) == EINVAL
+    assert L.sdp4_fill_f32(A, 0, 1.0, None) == OK
+
+
+@pytest.mark.cpu_only
 def test_element_counts_beyond_the_limit_are_rejected():
     big = (1 << 48) + 4096
     L = sdp4.lib()
@@ -201,6 +217,7 @@ def test_element_counts_beyond_the_limit_are_rejected():
     assert L.sdp4_grad_quant_sr(A, big, 8, 256, 128, 1, 0, B, CC, None) == EINVAL
     assert L.sdp4_hadamard(A, B, big, 256, None) == EINVAL
     assert L.sdp4_copy_f32(A, B, big, None) == EINVAL
+    assert L.sdp4_read_f32(A, big, B, None) == EINVAL and L.sdp4_fill_f32(A, big, 0.0, None) == EINVAL
     assert L.sdp4_codes_bytes(big, 8) == -1 and L.sdp4_num_groups(big, 128) == -1
     assert L.sdp4_codes_bytes(1 << 48, 8) == 1 << 48
 

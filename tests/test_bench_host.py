@@ -78,7 +78,28 @@ def test_all_cores_baseline_slices_the_sample(monkeypatch):
     import synth
     w = synth.WORKLOADS["c5"]
     monkeypatch.setattr(bench.os, "sched_getaffinity", lambda pid: set(range(3)))
-    r = bench.cpu_baseline_all_cores(w, 16, 0)
+    r = bench.cpu_baseline_all_cores(w, 1 << 16, 0)
     assert r["cores"] == 3 and r["kind"] == "oracle" and r["value"] > 0
     per = int(r["sample"].split(" slices of ")[1].split(",")[0])
     assert per % (w.P * w.Q * max(w.group, w.hadamard_block, w.qwd_group)) == 0 and 3 * per <= 1 << 16
+
+
+def test_read_write_split_and_additive_bound():
+    """Reads per launch are the inputs each kernel must load; the additive
+    bound lies between the write-only and the read-only rate and equals
+    either one for a pure stream."""
+    pytest.importorskip("torch")
+    from paper_2410_15526_amd.pipeline import HotPath
+    n, g, P, Q = 1_625_292_800, 128, 8, 4
+    info = HotPath.kernel_info(type("S", (), dict(n=n, group=g, qwd_group=g, P=P, Q=Q, M=n // P, m=n // P // Q,
+                                                   prev_dtype="bf16"))())
+    assert info["qwd_encode"].read_bytes == 6 * n
+    assert info["qwd_decode"].read_bytes == n // 2 + 8 * n // g + 2 * n
+    assert info["grad_quant"].read_bytes == 4 * n
+    assert info["reduce_intra"].read_bytes == n + 4 * n // g
+    assert info["reduce_inter"].read_bytes == n // P // 2 + 4 * n // P // g
+    c = {"read_GBps": 7000.0, "write_GBps": 6000.0}
+    assert bench.rw_additive_GBps(10, 0, c) == pytest.approx(7000.0)
+    assert bench.rw_additive_GBps(0, 10, c) == pytest.approx(6000.0)
+    assert 6000.0 < bench.rw_additive_GBps(1, 1, c) < 7000.0
+    assert bench.rw_additive_GBps(1, 1, c) == pytest.approx(2 / (1 / 7000 + 1 / 6000))

@@ -419,6 +419,25 @@ def test_reduce_f32_and_copy(P, n):
     assert np.array_equal(host(z), xs[0])
 
 
+@pytest.mark.parametrize("n", [4, 4099, 1 << 20, (1 << 22) + 7])
+def test_read_and_fill_yardsticks(n):
+    """The bandwidth yardsticks touch every element: the read stream's XOR
+    checksum (bit patterns of x[i] into word i % 4) and the fill's output."""
+    say(f"read/fill yardsticks n={n}")
+    t = torch()
+    r = np.random.default_rng(n)
+    x = r.standard_normal(n).astype(np.float32)
+    sink = t.zeros(4, dtype=t.int32, device="cuda")
+    sdp4.sdp4_read_f32(dev(x), sink)
+    y = empty(n, "f32")
+    sdp4.sdp4_fill_f32(y, -2.75)
+    sync()
+    b = x.view(np.uint32)
+    want = np.array([np.bitwise_xor.reduce(b[k::4]) if b[k::4].size else 0 for k in range(4)], np.uint32)
+    assert np.array_equal(host(sink).view(np.uint32), want)
+    assert np.all(host(y) == np.float32(-2.75))
+
+
 # ----------------------------------------------------------------------------
 # the two-level chain, run the way one GPU runs it
 # ----------------------------------------------------------------------------
