@@ -142,6 +142,10 @@
 #ifndef SDP4_ENC_EARLY_LOAD_BF16
 #define SDP4_ENC_EARLY_LOAD_BF16 0 // the same for bf16 weights
 #endif
+#ifndef SDP4_ENC_FLUSH_PCT
+#define SDP4_ENC_FLUSH_PCT 10 // phased encoder: a buffer that fills with more than this share of the period
+                              // left to read is written out at once (else the wave sleeps to the write phase)
+#endif
 #ifndef SDP4_ENC_HALF_T
 #define SDP4_ENC_HALF_T 1 // encoder: transpose its inputs through an LDS region of half a tile
 #endif
@@ -227,8 +231,8 @@ SDP4_DEV int tile_valid(int64_t n, int64_t base, int W) { return (int)(n - base 
 // system would otherwise idle; later tiles compute first, keeping one load
 // in flight per wave.
 template <int DEPTH, int WPB, bool EARLY, class Tile, class Load, class Proc, class Flush>
-SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_t read_ticks, Load load, Proc proc,
-                               Flush flush)
+SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_t read_ticks, uint64_t flush_ticks,
+                               Load load, Proc proc, Flush flush)
 {
     static_assert(DEPTH >= 1, "depth");
     const int wave = threadIdx.x / kWave;
@@ -273,14 +277,16 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
                     ++nbuf;
                     t += stride;
                     break;
-                } else if (nbuf > 0 && (!reading || !have)) {
+                } else if (nbuf > 0 && (!reading || !have || (nbuf == cap && read_ticks - (now - start) > flush_ticks))) {
+                    // write phase, no tile left, or a full buffer with more than flush_ticks of the read
+                    // phase left (with less, a short sleep costs less than writes amid the reads)
                     flush(nbuf);
                     nbuf = 0;
                     fresh = true;
                 } else if (!have) {
                     return; // no tile left and the buffer is empty
                 } else {
-                    __builtin_amdgcn_s_sleep(1); // buffer full in a read phase, or empty in a write phase
+                    __builtin_amdgcn_s_sleep(1); // empty buffer in a write phase (or full in a read phase)
                     fresh = true;
                 }
             }
@@ -502,7 +508,11 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
         };
         // early loads measured faster with float32 model weights only
         constexpr bool EARLY = BF16 ? SDP4_ENC_EARLY_LOAD_BF16 : SDP4_ENC_EARLY_LOAD_F32;
-        phased_tile_loop<kEncPhaseDepth, WPB, EARLY, Tile>(ntiles, CAP, period, read_ticks, load, proc, flush);
+        // a buffer that fills with more than SDP4_ENC_FLUSH_PCT per cent of the period left to read is
+        // written out at once
+        const uint64_t flush_ticks = period * SDP4_ENC_FLUSH_PCT / 100;
+        phased_tile_loop<kEncPhaseDepth, WPB, EARLY, Tile>(ntiles, CAP, period, read_ticks, flush_ticks, load, proc,
+                                                           flush);
     }
 }
 
