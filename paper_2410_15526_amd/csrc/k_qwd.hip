@@ -39,6 +39,14 @@ int qwd_encode_e(const float *w_new, const void *w_prev, bool bf16, bool sym, in
         if (read_ticks == 0 || read_ticks >= period)
             period = read_ticks = 0;
     }
+    if (period == 0) { // streaming: the instantiation without the phased mode's LDS buffers
+        auto ks = bf16 ? (sym ? k_qwd_encode<true, true, E, kDepth, WPB, 128, false>
+                              : k_qwd_encode<true, false, E, kDepth, WPB, 128, false>)
+                       : (sym ? k_qwd_encode<false, true, E, kDepth, WPB, 128, false>
+                              : k_qwd_encode<false, false, E, kDepth, WPB, 128, false>);
+        return launch<WPB>(ks, wave_blocks<WPB>(n, E), kEncStreamCap, s, w_new, w_prev, n, group, codes, scale, minv,
+                           period, read_ticks);
+    }
     return launch<WPB>(k, wave_blocks<WPB>(n, E), kEncCap, s, w_new, w_prev, n, group, codes, scale, minv, period,
                        read_ticks);
 }

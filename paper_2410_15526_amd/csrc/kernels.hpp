@@ -75,7 +75,10 @@
 #define SDP4_ENC_WAVES 4
 #endif
 #ifndef SDP4_ENC_BPC
-#define SDP4_ENC_BPC 1
+#define SDP4_ENC_BPC 1 // the clock-phased encoder
+#endif
+#ifndef SDP4_ENC_STREAM_BPC
+#define SDP4_ENC_STREAM_BPC -2 // the streaming encoder (launches that are not phased), without the phased LDS buffers
 #endif
 #ifndef SDP4_K1_WAVES
 #define SDP4_K1_WAVES 8 // K1 with 16 elements per lane
@@ -351,7 +354,7 @@ SDP4_DEV void fused_fwht(float (&v)[E], float cn, int el)
 // (codes 0..15, scale and minimum) or, with SYM, symmetric (codes -7..7,
 // scale only; minv is not touched)
 // ---------------------------------------------------------------------------
-template <bool BF16, bool SYM, int E, int DEPTH, int WPB, int PMIN = 128>
+template <bool BF16, bool SYM, int E, int DEPTH, int WPB, int PMIN = 128, bool PHASE = true>
 __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     const float *__restrict__ w_new, const void *__restrict__ w_prev, int64_t n, int group,
     uint8_t *__restrict__ codes, float *__restrict__ scale, float *__restrict__ minv, uint64_t period,
@@ -362,16 +365,17 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     constexpr int RP = BF16 ? E / 8 : E / 4;       // previous-weight chunks per lane
     // Phased mode (E = 32: one 16-byte code chunk per lane and tile) buffers
     // CAP tiles per wave: codes, then scales and minima of up to HMAX groups
-    // (groups of at least PMIN elements).
-    constexpr bool PHASED = E == 32;
+    // (groups of at least PMIN elements).  PHASE = false: the streaming form
+    // only, without the buffers' LDS (so that more blocks fit a CU).
+    constexpr bool PHASED = E == 32 && PHASE;
     constexpr int CAP = PHASED ? enc_phase_cap(PMIN) : 1;
     constexpr int HMAX = W / PMIN;
     // inputs of 8 chunks per lane pass through the LDS in two halves
     constexpr bool HALFT = SDP4_ENC_HALF_T && R == 8;
     __shared__ u32x4 lds_all[WPB][kWave * (HALFT ? R / 2 : R)];
-    __shared__ u32x4 cbuf_all[WPB][CAP * kWave];
-    __shared__ float hbuf_all[WPB][CAP * 2 * HMAX];
-    __shared__ int64_t tbuf_all[WPB][CAP];
+    __shared__ u32x4 cbuf_all[PHASED ? WPB : 1][PHASED ? CAP * kWave : 1];
+    __shared__ float hbuf_all[PHASED ? WPB : 1][PHASED ? CAP * 2 * HMAX : 1];
+    __shared__ int64_t tbuf_all[PHASED ? WPB : 1][PHASED ? CAP : 1];
     const int wv = threadIdx.x / kWave;
     u32x4 *lds = lds_all[wv];
     const int lane = lane_id();
@@ -452,6 +456,9 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_encode(
     };
     const int64_t ntiles = (n + W - 1) / W;
     if (!PHASED || period == 0) { // ordinary stream: each tile's output is stored at once
+        (void)cbuf_all;
+        (void)hbuf_all;
+        (void)tbuf_all;
         auto proc = [&](int64_t t, Tile &in) {
             const int64_t base = t * W;
             const int valid = tile_valid(n, base, W);
@@ -838,7 +845,7 @@ int64_t wave_blocks(int64_t n, int E)
 }
 
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
-constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC;
+constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC, kEncStreamCap = SDP4_ENC_STREAM_BPC;
 constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
 constexpr int kK1SrCap = SDP4_K1_SR_BPC;
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
