@@ -337,6 +337,14 @@ def main():
         torch.cuda.synchronize()
         return round(a.elapsed_time(b) / reps, 4)
 
+    # each step kernel alone over back-to-back launches (no event pair per launch, whose ~5 us of
+    # dispatch and event processing is a visible share of the short kernels)
+    for name, fn in hp.launches():
+        ms = timed(lambda: fn(None), reps=10)
+        gbps = info[name].alg_bytes / (ms * 1e-3) / 1e9
+        kernels[name]["ms_isolated"] = ms
+        kernels[name]["hbm_frac_isolated"] = round(gbps / HBM_PEAK_GBPS, 4)
+
     # read-only / write-only / copy ceilings at the step's array size, and each kernel against the
     # bound its own mix of reads and writes would have at those rates
     ceil = None
