@@ -208,6 +208,19 @@ def rw_additive_GBps(read_bytes: int, write_bytes: int, c: dict) -> float:
     return (read_bytes + write_bytes) / t / 1e9
 
 
+def workload_from_args(args):
+    """The named workload with any shape overrides from the command line."""
+    from dataclasses import replace
+    import synth
+    w = synth.WORKLOADS[args.workload]
+    over = {k: v for k, v in (("n", args.n), ("group", args.group), ("hadamard_block", args.hblock), ("P", args.P),
+                              ("Q", args.Q), ("qwd_group", args.qwd_group), ("prev_dtype", args.model_weights))
+            if v is not None}
+    if over:
+        w = replace(w, extra_groups=(), extra_qwd_groups=(), **over)
+    return w
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -223,6 +236,14 @@ def main():
     ap.add_argument("--no-standalone", action="store_true")
     ap.add_argument("--no-group-sweep", action="store_true")
     ap.add_argument("--no-ceilings", action="store_true")
+    # overrides of the workload's shape (the recipe of its data stays that of --workload)
+    ap.add_argument("--n", type=int, default=None, help="element count of the shard")
+    ap.add_argument("--group", type=int, default=None, help="gradient quantization group")
+    ap.add_argument("--hblock", type=int, default=None, help="Hadamard block (0 = none)")
+    ap.add_argument("--P", type=int, default=None, help="chunks of the 8-bit dequantize-reduce")
+    ap.add_argument("--Q", type=int, default=None, help="chunks of the 4-bit dequantize-reduce")
+    ap.add_argument("--qwd-group", type=int, default=None, help="qWD quantization group")
+    ap.add_argument("--model-weights", choices=("f32", "bf16"), default=None)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -237,7 +258,7 @@ def main():
     from paper_2410_15526_amd import sdp4
     from paper_2410_15526_amd.pipeline import HotPath
 
-    w = synth.WORKLOADS[args.workload]
+    w = workload_from_args(args)
     torch.cuda.set_device(0)
     hp = HotPath(w.n, w.group, w.hadamard_block, w.P, w.Q, w.qwd_group, w.prev_dtype)
     t_fill = time.perf_counter()
@@ -453,7 +474,8 @@ def main():
             standalone["reduce_inter"]["vs_rw_additive"] = round(gbps / rw_additive_GBps(rd, alg - rd, ceil), 4)
         del c4, s4, out, cl, sl
 
-    traffic = traffic_for(dom, args.workload)
+    # the recorded counters hold for the named workload's own shape only
+    traffic = traffic_for(dom, args.workload if w is synth.WORKLOADS[args.workload] else "custom shape")
     line = {
         "metric": METRIC,
         "value": round(value, 1),

@@ -103,3 +103,17 @@ def test_read_write_split_and_additive_bound():
     assert bench.rw_additive_GBps(0, 10, c) == pytest.approx(6000.0)
     assert 6000.0 < bench.rw_additive_GBps(1, 1, c) < 7000.0
     assert bench.rw_additive_GBps(1, 1, c) == pytest.approx(2 / (1 / 7000 + 1 / 6000))
+
+
+def test_workload_overrides():
+    """Shape overrides replace the named workload's fields (and drop its extra sweeps)."""
+    import argparse
+    a = argparse.Namespace(workload="c4", n=1 << 20, group=64, hblock=0, P=4, Q=2, qwd_group=256,
+                           model_weights="f32")
+    w = bench.workload_from_args(a)
+    assert (w.n, w.group, w.hadamard_block, w.P, w.Q, w.qwd_group, w.prev_dtype) == (1 << 20, 64, 0, 4, 2, 256, "f32")
+    assert w.extra_groups == () and w.extra_qwd_groups == () and w.wid == 4
+    b = argparse.Namespace(workload="c4", n=None, group=None, hblock=None, P=None, Q=None, qwd_group=None,
+                           model_weights=None)
+    import synth
+    assert bench.workload_from_args(b) is synth.WORKLOADS["c4"]
