@@ -29,6 +29,7 @@
 namespace sdp4 {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 #ifndef SDP4_WAVES_PER_BLOCK
 #define SDP4_WAVES_PER_BLOCK 4

@@ -43,17 +43,23 @@
 #endif
 // Elements per lane of each kernel family (32 or 64, and 16 for the 8-bit K1;
 // group 4096 always uses 64).
-#ifndef SDP4_E_ENC
-#define SDP4_E_ENC 32
+#ifndef SDP4_E_ENC_STREAM
+#define SDP4_E_ENC_STREAM 16 // the streaming qWD encoder (16 or 32; the phased one takes 32)
 #endif
-#ifndef SDP4_E_DEC
-#define SDP4_E_DEC 32
+#ifndef SDP4_E_DEC_BF16
+#define SDP4_E_DEC_BF16 16 // qWD decode, bf16 model weights
+#endif
+#ifndef SDP4_E_DEC_F32
+#define SDP4_E_DEC_F32 8 // qWD decode, float32 model weights
 #endif
 #ifndef SDP4_E_K1
 #define SDP4_E_K1 16 // 8-bit K1 only: 4-bit codes need 32 per lane to fill a 16-byte store
 #endif
 #ifndef SDP4_E_RED
 #define SDP4_E_RED 32
+#endif
+#ifndef SDP4_E_K3
+#define SDP4_E_K3 32 // dequantize-reduce of 4-bit messages to float32 (K3): 16 or 32 elements per lane
 #endif
 #ifndef SDP4_E_RQ8
 // Elements per lane of the re-quantizing dequantize-reduce of 8-bit messages,
@@ -78,7 +84,7 @@
 #define SDP4_ENC_BPC 1 // the clock-phased encoder
 #endif
 #ifndef SDP4_ENC_STREAM_BPC
-#define SDP4_ENC_STREAM_BPC -2 // the streaming encoder (launches that are not phased), without the phased LDS buffers
+#define SDP4_ENC_STREAM_BPC -4 // the streaming encoder (launches that are not phased), without the phased LDS buffers
 #endif
 #ifndef SDP4_K1_WAVES
 #define SDP4_K1_WAVES 8 // K1 with 16 elements per lane
@@ -103,7 +109,7 @@
 #define SDP4_DEC_WAVES 4
 #endif
 #ifndef SDP4_DEC_BPC
-#define SDP4_DEC_BPC -2
+#define SDP4_DEC_BPC -4
 #endif
 #ifndef SDP4_RQ_WAVES
 #define SDP4_RQ_WAVES 4
@@ -131,7 +137,7 @@
 #define SDP4_ENC_READ_PCT 92 // per cent of the period spent reading
 #endif
 #ifndef SDP4_ENC_PHASE_US_F32
-#define SDP4_ENC_PHASE_US_F32 90 // the same with float32 model weights (a tile reads a third more)
+#define SDP4_ENC_PHASE_US_F32 0 // the same with float32 model weights (0: they stream, measured faster)
 #endif
 #ifndef SDP4_ENC_READ_PCT_F32
 #define SDP4_ENC_READ_PCT_F32 94
@@ -305,7 +311,6 @@ template <int E, int BITS>
 SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, const uint32_t (&q)[E], int el)
 {
     if constexpr (E * BITS == 64) { // 16 nibbles: 8 bytes per lane, 512 contiguous bytes per wave
-        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
         if (E * el < valid)
             __builtin_nontemporal_store(u32x2{pack_nibbles8(q), pack_nibbles8(q + 8)},
                                         reinterpret_cast<u32x2 *>(dst) + el);
@@ -533,14 +538,16 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_decode(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const float *__restrict__ minv, int64_t n, int group, void *__restrict__ w_prev)
 {
+    static_assert(E == 8 || E == 16 || E % 32 == 0, "lane slice");
     constexpr int W = kWave * E;
-    constexpr int RP = BF16 ? E / 8 : E / 4;
+    constexpr int RP = BF16 ? E / 8 : E / 4;   // 16-byte chunks of weights per lane
+    constexpr int CWD = E / 8;                 // 32-bit words of codes per lane
     __shared__ u32x4 lds_all[WPB][kWave * (E / 4)];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
     const int gs = group_shift(group);
     struct Tile {
-        u32x4 c[E / 32];
+        uint32_t c[CWD];
         float s, mn;
         u32x4 w[RP];
     };
@@ -549,17 +556,30 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_decode(
         const int valid = tile_valid(n, base, W);
         const int off = E * lane;
         if (off < valid) {
-            const u32x4 *src = reinterpret_cast<const u32x4 *>(codes + (base + off) / 2);
+            const uint8_t *src = codes + (base + off) / 2;
+            if constexpr (CWD >= 4) {
 #pragma unroll
-            for (int k = 0; k < E / 32; ++k)
-                in.c[k] = __builtin_nontemporal_load(src + k);
+                for (int k = 0; k < CWD / 4; ++k) {
+                    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src) + k);
+                    in.c[4 * k] = v.x;
+                    in.c[4 * k + 1] = v.y;
+                    in.c[4 * k + 2] = v.z;
+                    in.c[4 * k + 3] = v.w;
+                }
+            } else if constexpr (CWD == 2) {
+                const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(src));
+                in.c[0] = v.x;
+                in.c[1] = v.y;
+            } else {
+                in.c[0] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(src));
+            }
             const int64_t gi = (base + off) >> gs;
             in.s = scale[gi];
             in.mn = SYM ? 0.0f : minv[gi];
         } else {
 #pragma unroll
-            for (int k = 0; k < E / 32; ++k)
-                in.c[k] = u32x4{0u, 0u, 0u, 0u};
+            for (int k = 0; k < CWD; ++k)
+                in.c[k] = 0u;
             in.s = 0.0f;
             in.mn = 0.0f;
         }
@@ -581,8 +601,8 @@ __global__ __launch_bounds__(kWave * WPB) void k_qwd_decode(
         else
             chunks_to_f32<E>(c, w);
 #pragma unroll
-        for (int k = 0; k < E / 8; ++k) { // word k: the nibbles of elements 8k .. 8k+7, even ones low
-            const uint32_t word = in.c[k / 4][k % 4];
+        for (int k = 0; k < CWD; ++k) { // word k: the nibbles of elements 8k .. 8k+7, even ones low
+            const uint32_t word = in.c[k];
             if constexpr (SYM) {
 #pragma unroll
                 for (int m = 0; m < 8; ++m) {
@@ -685,7 +705,10 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
 {
     constexpr int W = kWave * E;
     constexpr int R = E / 4;
-    constexpr int CW = E * BITS_IN / 128; // input chunks (16 B) per lane per peer
+    // input chunks (16 B) per lane per peer; HALF: 8 bytes (16 elements of 4-bit codes), kept in a
+    // chunk's first two words
+    constexpr bool HALF = E * BITS_IN == 64;
+    constexpr int CW = HALF ? 1 : E * BITS_IN / 128;
     __shared__ u32x4 lds_all[WPB][kWave * R];
     u32x4 *lds = lds_all[threadIdx.x / kWave];
     const int lane = lane_id();
@@ -713,11 +736,15 @@ __global__ __launch_bounds__(kWave * WPB) void k_dequant_reduce(
                 continue;
             }
             if (j < P && active) {
-                const u32x4 *src = reinterpret_cast<const u32x4 *>(
-                    static_cast<const uint8_t *>(peers.codes[j]) + (base + off) * BITS_IN / 8);
+                const uint8_t *src = static_cast<const uint8_t *>(peers.codes[j]) + (base + off) * BITS_IN / 8;
+                if constexpr (HALF) {
+                    const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(src));
+                    in.c[j][0] = u32x4{v.x, v.y, 0u, 0u};
+                } else {
 #pragma unroll
-                for (int k = 0; k < CW; ++k)
-                    in.c[j][k] = __builtin_nontemporal_load(src + k);
+                    for (int k = 0; k < CW; ++k)
+                        in.c[j][k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src) + k);
+                }
                 in.s[j] = peers.scales[j][gi];
             } else {
 #pragma unroll

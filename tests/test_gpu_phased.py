@@ -1,7 +1,9 @@
-"""The qWD encoder's phased mode (large launches: loads only in the read part
-of a clock period, outputs buffered in LDS and written in the rest) against
-the oracle on every element: groups 64..1024, both codecs, float32 and
-bfloat16 model weights, and a shard whose last wave tile is partial.  The
+"""The qWD encoder's phased mode (large launches with bfloat16 model weights:
+loads only in the read part of a clock period, outputs buffered in LDS and
+written in the rest) against the oracle on every element: groups 64..1024,
+both codecs, and a shard whose last wave tile is partial.  Float32 model
+weights stream at every size, so their cases check the streaming encoder at
+the same size.  The
 8-bit K1 and the 4-bit re-quantizing dequantize-reduce (K2: 8- and 4-bit peer
 messages, 2..16 peers) are checked at the same size; they stream without
 phases."""
@@ -29,7 +31,8 @@ def inputs(bf16, seed):
     return new, prev
 
 
-@pytest.mark.parametrize("bf16,group", [(True, 64), (False, 64), (True, 128), (False, 256), (True, 512), (False, 1024)])
+@pytest.mark.parametrize("bf16,group", [(True, 64), (False, 64), (True, 128), (True, 256), (False, 256), (True, 512),
+                                        (True, 1024), (False, 1024)])
 def test_phased_asymmetric_encode_matches_oracle(bf16, group):
     say(f"phased qwd encode bf16={bf16} group={group} n={N}")
     new, prev = inputs(bf16, group)
