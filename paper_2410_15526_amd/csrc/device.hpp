@@ -402,13 +402,32 @@ SDP4_DEV int element_lane(int p)
                    "+v"(w[7]), "+v"(w[8]), "+v"(w[9]), "+v"(w[10]), "+v"(w[11]), "+v"(w[12]), "+v"(w[13]),      \
                    "+v"(w[14]), "+v"(w[15])                                                                     \
                  : "v"(s))
+// The same for a lane slice of 8 elements.
+#define SDP4_FMAC_DPP_I8(i, CTRL) "v_fmac_f32_dpp %" #i ", %" #i ", %8 " CTRL " row_mask:0xf bank_mask:0xf\n\t"
+#define SDP4_FMAC_DPP_8(CTRL, w, s)                                                                              \
+    asm volatile("s_nop 4\n\t" SDP4_FMAC_DPP_I8(0, CTRL) SDP4_FMAC_DPP_I8(1, CTRL) SDP4_FMAC_DPP_I8(2, CTRL)     \
+                     SDP4_FMAC_DPP_I8(3, CTRL) SDP4_FMAC_DPP_I8(4, CTRL) SDP4_FMAC_DPP_I8(5, CTRL)              \
+                         SDP4_FMAC_DPP_I8(6, CTRL) SDP4_FMAC_DPP_I8(7, CTRL)                                    \
+                 : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]), "+v"(w[4]), "+v"(w[5]), "+v"(w[6]),         \
+                   "+v"(w[7])                                                                                   \
+                 : "v"(s))
 
 template <int E, int D>
 SDP4_DEV void fwht_cross_signed(float (&v)[E], int el)
 {
-    static_assert(E % 16 == 0, "lane slice");
+    static_assert(E % 8 == 0, "lane slice");
     const float sg = (el & D) ? -1.0f : 1.0f;
-    if constexpr (D <= 8) {
+    if constexpr (D <= 8 && E % 16 != 0) {
+        float(&w)[8] = *reinterpret_cast<float(*)[8]>(v);
+        if constexpr (D == 1)
+            SDP4_FMAC_DPP_8("quad_perm:[1,0,3,2]", w, sg);
+        else if constexpr (D == 2)
+            SDP4_FMAC_DPP_8("quad_perm:[2,3,0,1]", w, sg);
+        else if constexpr (D == 4)
+            SDP4_FMAC_DPP_8("row_half_mirror", w, sg);
+        else
+            SDP4_FMAC_DPP_8("row_ror:8", w, sg);
+    } else if constexpr (D <= 8) {
 #pragma unroll
         for (int b = 0; b < E / 16; ++b) {
             float(&w)[16] = *reinterpret_cast<float(*)[16]>(v + 16 * b);

@@ -23,7 +23,14 @@ struct GradQuant {
             return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, uint64_t(0),
                                uint64_t(0));
         }
-        if (bits == 8 && SDP4_E_K1 == 16 && group <= kWave * 16) {   // a group must fit one wavefront
+        if constexpr (NB <= kWave * 8) { // a Hadamard block must fit one wavefront
+            if (bits == 8 && SDP4_E_K1 == 8 && group <= kWave * 8) { // and so must a group
+                constexpr int WPB = kK1Waves8;
+                return launch<WPB>(k_grad_quant<8, 8, NB, kDepth, WPB>, wave_blocks<WPB>(n, 8), kK1Cap8, s, x, n, group,
+                                   cn, codes, scale, uint64_t(0), uint64_t(0));
+            }
+        }
+        if (bits == 8 && (SDP4_E_K1 == 8 || SDP4_E_K1 == 16) && group <= kWave * 16) { // a group must fit one wavefront
             constexpr int WPB = kK1Waves;
             return launch<WPB>(k_grad_quant<8, 16, NB, kDepth, WPB>, wave_blocks<WPB>(n, 16), kK1Cap, s, x, n, group, cn,
                                codes, scale, uint64_t(0), uint64_t(0));

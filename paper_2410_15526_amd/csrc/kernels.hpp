@@ -53,7 +53,7 @@
 #define SDP4_E_DEC_F32 8 // qWD decode, float32 model weights
 #endif
 #ifndef SDP4_E_K1
-#define SDP4_E_K1 16 // 8-bit K1 only: 4-bit codes need 32 per lane to fill a 16-byte store
+#define SDP4_E_K1 16 // 8-bit K1 only (8 or 16): 4-bit codes need 32 per lane to fill a 16-byte store
 #endif
 #ifndef SDP4_E_RED
 #define SDP4_E_RED 32
@@ -88,6 +88,12 @@
 #endif
 #ifndef SDP4_K1_WAVES
 #define SDP4_K1_WAVES 8 // K1 with 16 elements per lane
+#endif
+#ifndef SDP4_K1_WAVES_8
+#define SDP4_K1_WAVES_8 4 // K1 with 8 elements per lane
+#endif
+#ifndef SDP4_K1_BPC_8
+#define SDP4_K1_BPC_8 -8
 #endif
 #ifndef SDP4_K1_WAVES_32
 #define SDP4_K1_WAVES_32 8 // K1 with 32 elements per lane (4-bit codes, stochastic rounding)
@@ -310,10 +316,16 @@ SDP4_DEV void phased_tile_loop(int64_t ntiles, int cap, uint64_t period, uint64_
 template <int E, int BITS>
 SDP4_DEV void store_codes(uint8_t *__restrict__ dst, int valid, u32x4 *lds, const uint32_t (&q)[E], int el)
 {
-    if constexpr (E * BITS == 64) { // 16 nibbles: 8 bytes per lane, 512 contiguous bytes per wave
-        if (E * el < valid)
-            __builtin_nontemporal_store(u32x2{pack_nibbles8(q), pack_nibbles8(q + 8)},
-                                        reinterpret_cast<u32x2 *>(dst) + el);
+    if constexpr (E * BITS == 64) { // 16 nibbles or 8 bytes per lane: 512 contiguous bytes per wave
+        if (E * el < valid) {
+            if constexpr (BITS == 4)
+                __builtin_nontemporal_store(u32x2{pack_nibbles8(q), pack_nibbles8(q + 8)},
+                                            reinterpret_cast<u32x2 *>(dst) + el);
+            else
+                __builtin_nontemporal_store(
+                    u32x2{pack_bytes4(q[0], q[1], q[2], q[3]), pack_bytes4(q[4], q[5], q[6], q[7])},
+                    reinterpret_cast<u32x2 *>(dst) + el);
+        }
     } else {
         constexpr int RC = E * BITS / 128; // 16-byte chunks per lane
         u32x4 pk[RC];
@@ -875,6 +887,7 @@ constexpr int kCap = SDP4_BLOCKS_PER_CU;
 constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC, kEncStreamCap = SDP4_ENC_STREAM_BPC;
 constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
 constexpr int kK1SrCap = SDP4_K1_SR_BPC;
+constexpr int kK1Waves8 = SDP4_K1_WAVES_8, kK1Cap8 = SDP4_K1_BPC_8;
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
