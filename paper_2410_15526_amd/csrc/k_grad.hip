@@ -48,9 +48,12 @@ struct Hadamard {
     {
         if constexpr (NB < 2)
             return 1;
+        else if constexpr (SDP4_E_HAD == 16 && NB <= kWave * 16)
+            return launch<kWavesPerBlock>(k_hadamard<16, NB, kDepth, kWavesPerBlock>, wave_blocks<kWavesPerBlock>(n, 16),
+                                          kHadCap, s, x, y, n, cn);
         else
             return launch<kWavesPerBlock>(k_hadamard<32, NB, kDepth, kWavesPerBlock>, wave_blocks<kWavesPerBlock>(n, 32),
-                                          kCap, s, x, y, n, cn);
+                                          kHadCap, s, x, y, n, cn);
     }
 };
 

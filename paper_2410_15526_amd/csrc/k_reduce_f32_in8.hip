@@ -13,6 +13,8 @@ struct DequantReduceF32 {
     {
         if (use_wide_lanes(group, SDP4_E_RED))
             return dr_launch<8, 0, 64, NB>(peers, P, n, group, cn, out_scale, nullptr, nullptr, out_f32, s);
+        if constexpr (SDP4_E_RF8 == 16 && NB <= kWave * 16)
+            return dr_launch<8, 0, 16, NB>(peers, P, n, group, cn, out_scale, nullptr, nullptr, out_f32, s);
         return dr_launch<8, 0, 32, NB>(peers, P, n, group, cn, out_scale, nullptr, nullptr, out_f32, s);
     }
 };

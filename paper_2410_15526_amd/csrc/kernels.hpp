@@ -61,6 +61,15 @@
 #ifndef SDP4_E_K3
 #define SDP4_E_K3 32 // dequantize-reduce of 4-bit messages to float32 (K3): 16 or 32 elements per lane
 #endif
+#ifndef SDP4_E_RF8
+#define SDP4_E_RF8 16 // dequantize-reduce of 8-bit messages to float32: 16 or 32 elements per lane
+#endif
+#ifndef SDP4_E_HAD
+#define SDP4_E_HAD 16 // the standalone Hadamard transform: 16 or 32 elements per lane
+#endif
+#ifndef SDP4_HAD_BPC
+#define SDP4_HAD_BPC -4
+#endif
 #ifndef SDP4_E_RQ8
 // Elements per lane of the re-quantizing dequantize-reduce of 8-bit messages,
 // deterministic or stochastically rounded (16: one 16-byte chunk per peer and
@@ -889,6 +898,7 @@ constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = 
 constexpr int kK1SrCap = SDP4_K1_SR_BPC;
 constexpr int kK1Waves8 = SDP4_K1_WAVES_8, kK1Cap8 = SDP4_K1_BPC_8;
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
+constexpr int kHadCap = SDP4_HAD_BPC;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
 constexpr int kRq8Waves = SDP4_RQ8_WAVES, kRq8Cap = SDP4_RQ8_BPC;
