@@ -16,6 +16,13 @@ struct GradQuantSR {
             auto k = bits == 8 ? k_grad_quant<8, 64, NB, kDepth, WPB, true> : k_grad_quant<4, 64, NB, kDepth, WPB, true>;
             return launch<WPB>(k, wave_blocks<WPB>(n, 64), kK1SrCap, s, x, n, group, cn, codes, scale, seed, offset);
         }
+        if constexpr (SDP4_E_K1_SR == 16 && NB <= kWave * 16) {
+            if (bits == 8 && group <= kWave * 16) { // 8-bit codes, a group within one wavefront
+                constexpr int WPB = kK1Sr16Waves;
+                return launch<WPB>(k_grad_quant<8, 16, NB, kDepth, WPB, true>, wave_blocks<WPB>(n, 16), kK1Sr16Cap, s,
+                                   x, n, group, cn, codes, scale, seed, offset);
+            }
+        }
         constexpr int WPB = kK1Waves32;
         auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth, WPB, true> : k_grad_quant<4, 32, NB, kDepth, WPB, true>;
         return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1SrCap, s, x, n, group, cn, codes, scale, seed, offset);

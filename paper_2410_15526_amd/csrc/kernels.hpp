@@ -110,8 +110,17 @@
 #ifndef SDP4_K1_WAVES_PLAIN
 #define SDP4_K1_WAVES_PLAIN 4 // K1 without a transform (32 elements per lane)
 #endif
+#ifndef SDP4_E_K1_SR
+#define SDP4_E_K1_SR 16 // K1 with stochastic rounding, 8-bit codes: 16 or 32 elements per lane
+#endif
+#ifndef SDP4_K1_SR16_WAVES
+#define SDP4_K1_SR16_WAVES 4 // ... with 16 elements per lane: a full grid of 4-wave blocks
+#endif
+#ifndef SDP4_K1_SR16_BPC
+#define SDP4_K1_SR16_BPC -64
+#endif
 #ifndef SDP4_K1_SR_BPC
-#define SDP4_K1_SR_BPC 1 // K1 with stochastic rounding: one persistent block per compute unit
+#define SDP4_K1_SR_BPC 1 // K1 with stochastic rounding, 32 or 64 per lane: one persistent block per compute unit
 #endif
 #ifndef SDP4_K1_BPC
 #define SDP4_K1_BPC -3
@@ -137,6 +146,12 @@
 #endif
 #ifndef SDP4_RQ8_BPC
 #define SDP4_RQ8_BPC -2
+#endif
+#ifndef SDP4_RQ8_SR_WAVES // ... the same with stochastic rounding
+#define SDP4_RQ8_SR_WAVES 8
+#endif
+#ifndef SDP4_RQ8_SR_BPC
+#define SDP4_RQ8_SR_BPC -64
 #endif
 #ifndef SDP4_RF_WAVES
 #define SDP4_RF_WAVES 4
@@ -895,13 +910,13 @@ int64_t wave_blocks(int64_t n, int E)
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
 constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC, kEncStreamCap = SDP4_ENC_STREAM_BPC;
 constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
-constexpr int kK1SrCap = SDP4_K1_SR_BPC;
+constexpr int kK1SrCap = SDP4_K1_SR_BPC, kK1Sr16Waves = SDP4_K1_SR16_WAVES, kK1Sr16Cap = SDP4_K1_SR16_BPC;
 constexpr int kK1Waves8 = SDP4_K1_WAVES_8, kK1Cap8 = SDP4_K1_BPC_8;
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
 constexpr int kHadCap = SDP4_HAD_BPC;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
-constexpr int kRq8Waves = SDP4_RQ8_WAVES, kRq8Cap = SDP4_RQ8_BPC;
+constexpr int kRq8Waves = SDP4_RQ8_WAVES, kRq8Cap = SDP4_RQ8_BPC, kRq8SrWaves = SDP4_RQ8_SR_WAVES, kRq8SrCap = SDP4_RQ8_SR_BPC;
 
 // 64 elements per lane: required for groups of 4096 (a group must fit one
 // wavefront), allowed (preferred_e == 64) for any group of at least 64 (a
@@ -939,8 +954,8 @@ int dr_launch(const PeerTable &peers, int P, int64_t n, int group, float cn, flo
               uint64_t offset = 0)
 {
     constexpr int pipe = BITS_OUT == 0 ? kDepth : 0;
-    constexpr int WPB = BITS_OUT == 0 ? kRfWaves : E == 16 ? kRq8Waves : kRqWaves;
-    constexpr int cap = BITS_OUT == 0 ? kRfCap : E == 16 ? kRq8Cap : kRqCap;
+    constexpr int WPB = BITS_OUT == 0 ? kRfWaves : E == 16 ? (SR ? kRq8SrWaves : kRq8Waves) : kRqWaves;
+    constexpr int cap = BITS_OUT == 0 ? kRfCap : E == 16 ? (SR ? kRq8SrCap : kRq8Cap) : kRqCap;
     if (P <= 4)
         return launch<WPB>(k_dequant_reduce<BITS_IN, BITS_OUT, E, NB, 4, pipe, WPB, SR>, wave_blocks<WPB>(n, E), cap,
                            s, peers, P, n, group, cn, out_scale, out_codes, out_scales, out_f32, seed, offset);
