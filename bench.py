@@ -28,6 +28,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -60,17 +61,25 @@ def fill(dst, gen, n):
             dst[s:s + k].copy_(t)
 
 
+def _code_tokens(text: str) -> str:
+    """C/C++ source without its comments, whitespace runs collapsed (the
+    kernel sources hold no string literal with a comment marker in it)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_digest() -> str:
-    """Digest of the sources that decide what the kernels do on the device:
+    """Digest of the code that decides what the kernels do on the device:
     the kernels and their launch configuration (not the host-side argument
-    checks of the C ABI)."""
+    checks of the C ABI), comments and layout ignored."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2410_15526_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
         if f == "abi.cpp":
             continue
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(f.encode() + _code_tokens(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -15,21 +15,17 @@
 // on D.
 //
 // The SDP4_* macros below are build-time tuning knobs; their defaults are
-// the measured best on MI355X: one tile buffer per wave, 32 elements per lane
-// (16 for the 8-bit K1 with a transform and for the re-quantizing
-// dequantize-reduce of 8-bit messages, so that each lane loads one 16-byte
-// chunk per peer), and per kernel family a block shape and a grid mode.
-// Most kernels launch one block per work block, which the hardware
-// dispatches in address order, so the chip's accesses sweep memory front to
-// back (HBM serves that faster than the scattered fronts of a persistent
-// grid), with a cap on resident blocks per CU where that measured faster:
-// decode 2 blocks of four waves, K1 3 blocks of eight (of four without a
-// transform), K2 on 8-bit messages 2 blocks of eight, K3 and the rest 4
-// blocks of four.  The clock-phased qWD encoder (one block of four waves
-// per CU) and K1 with stochastic rounding (one block of eight) keep
-// persistent grids.  (How many bytes a CU keeps in flight, and how far
-// compute spreads its requests out, moves the mixed read/write bandwidth of
-// HBM by several per cent.)
+// the measured best on MI355X: one tile buffer per wave and, per kernel
+// family, a lane width E (8 to 64 elements per lane), a block shape and a
+// grid mode.  Most kernels launch one block per work block, which the
+// hardware dispatches in address order, so the chip's accesses sweep memory
+// front to back (HBM serves that faster than the scattered fronts of a
+// persistent grid), some with a cap on resident blocks per CU where that
+// measured faster.  The clock-phased qWD encoder (one block of four waves
+// per CU) and the stochastically rounded K1 with 4-bit codes keep persistent
+// grids.  (How many bytes a CU keeps in flight, and how far compute spreads
+// its requests out, moves the mixed read/write bandwidth of HBM by several
+// per cent.)
 #pragma once
 
 #include "device.hpp"
@@ -41,8 +37,7 @@
 #ifndef SDP4_PEER_LDS
 #define SDP4_PEER_LDS 1 // int8 peer chunks: coalesced loads + LDS transpose
 #endif
-// Elements per lane of each kernel family (32 or 64, and 16 for the 8-bit K1;
-// group 4096 always uses 64).
+// Elements per lane of each kernel family (groups of 4096 always take 64).
 #ifndef SDP4_E_ENC_STREAM
 #define SDP4_E_ENC_STREAM 16 // the streaming qWD encoder (16 or 32; the phased one takes 32)
 #endif

@@ -51,6 +51,19 @@ def test_source_digest_covers_device_sources_only(tmp_path, monkeypatch):
     assert bench.source_digest() != d0
 
 
+def test_source_digest_ignores_comments_and_layout(tmp_path, monkeypatch):
+    csrc = tmp_path / "paper_2410_15526_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    k = csrc / "kernels.hpp"
+    k.write_text("// header\nint f(int x) { return x + 1; }\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    d0 = bench.source_digest()
+    k.write_text("// another header\n/* a block\n   comment */\nint f(int x)\n{\n    return x + 1; // same\n}\n")
+    assert bench.source_digest() == d0
+    k.write_text("int f(int x) { return x + 2; }\n")     # the code changed
+    assert bench.source_digest() != d0
+
+
 def test_algorithmic_bytes_per_launch():
     """The per-element byte counts of the kernels (reads + writes, group 128,
     bf16 model weights), checked against the c5 shard's launches."""
