@@ -17,10 +17,15 @@ struct GradQuant {
             return launch<WPB>(k, wave_blocks<WPB>(n, 64), kCap, s, x, n, group, cn, codes, scale, uint64_t(0),
                                uint64_t(0));
         }
-        if constexpr (NB == 0) {   // no transform: 32 elements per lane, its own block shape
+        if constexpr (NB == 0) {   // no transform: its own lane width and block shape
             constexpr int WPB = kK1PlainWaves;
+            if (SDP4_E_K1_PLAIN == 16 && group <= kWave * 16) {
+                auto k = bits == 8 ? k_grad_quant<8, 16, 0, kDepth, WPB> : k_grad_quant<4, 16, 0, kDepth, WPB>;
+                return launch<WPB>(k, wave_blocks<WPB>(n, 16), kK1PlainCap, s, x, n, group, cn, codes, scale,
+                                   uint64_t(0), uint64_t(0));
+            }
             auto k = bits == 8 ? k_grad_quant<8, 32, 0, kDepth, WPB> : k_grad_quant<4, 32, 0, kDepth, WPB>;
-            return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, uint64_t(0),
+            return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1PlainCap, s, x, n, group, cn, codes, scale, uint64_t(0),
                                uint64_t(0));
         }
         if constexpr (NB <= kWave * 8) { // a Hadamard block must fit one wavefront

@@ -102,8 +102,14 @@
 #ifndef SDP4_K1_WAVES_32
 #define SDP4_K1_WAVES_32 8 // K1 with 32 elements per lane (4-bit codes, stochastic rounding)
 #endif
+#ifndef SDP4_E_K1_PLAIN
+#define SDP4_E_K1_PLAIN 16 // K1 without a transform: 16 or 32 elements per lane
+#endif
 #ifndef SDP4_K1_WAVES_PLAIN
-#define SDP4_K1_WAVES_PLAIN 4 // K1 without a transform (32 elements per lane)
+#define SDP4_K1_WAVES_PLAIN 4
+#endif
+#ifndef SDP4_K1_PLAIN_BPC
+#define SDP4_K1_PLAIN_BPC -6
 #endif
 #ifndef SDP4_E_K1_SR
 #define SDP4_E_K1_SR 16 // K1 with stochastic rounding, 8-bit codes: 16 or 32 elements per lane
@@ -907,7 +913,7 @@ constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC, kEncStreamCap 
 constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
 constexpr int kK1SrCap = SDP4_K1_SR_BPC, kK1Sr16Waves = SDP4_K1_SR16_WAVES, kK1Sr16Cap = SDP4_K1_SR16_BPC;
 constexpr int kK1Waves8 = SDP4_K1_WAVES_8, kK1Cap8 = SDP4_K1_BPC_8;
-constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN;
+constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN, kK1PlainCap = SDP4_K1_PLAIN_BPC;
 constexpr int kHadCap = SDP4_HAD_BPC;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
