@@ -628,7 +628,8 @@ def test_binding_reports_status():
 # ----------------------------------------------------------------------------
 
 @pytest.mark.parametrize("bits", [8, 4])
-@pytest.mark.parametrize("block,group", [(0, 32), (64, 128), (256, 128), (128, 512), (1024, 4096)])
+@pytest.mark.parametrize("block,group", [(0, 32), (64, 128), (256, 128), (128, 512), (512, 64), (1024, 256), (16, 1024),
+                                         (0, 2048), (1024, 4096)])
 @pytest.mark.parametrize("seed,offset", [(0, 0), (0xDEADBEEF12345678, 8 * 12345), (7, 1 << 33)])
 def test_grad_quant_sr(bits, block, group, seed, offset):
     n = size_for(max(group, block))
