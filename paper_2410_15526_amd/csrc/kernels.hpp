@@ -78,9 +78,9 @@
 #ifndef SDP4_BLOCKS_PER_CU
 #define SDP4_BLOCKS_PER_CU -4 // block cap of the kernels without one of their own below
 #endif
-// Block shape (waves per block, resident blocks per compute unit) of the qWD
-// encoder and of K1; every other kernel uses SDP4_WAVES_PER_BLOCK (device.hpp)
-// and SDP4_BLOCKS_PER_CU.
+// Block shapes (waves per block, block cap) of the qWD encoder and of the K1
+// variants; the standalone transform and the yardsticks use
+// SDP4_WAVES_PER_BLOCK (device.hpp) and caps of their own.
 #ifndef SDP4_ENC_WAVES
 #define SDP4_ENC_WAVES 4
 #endif
@@ -100,7 +100,7 @@
 #define SDP4_K1_BPC_8 -8
 #endif
 #ifndef SDP4_K1_WAVES_32
-#define SDP4_K1_WAVES_32 8 // K1 with 32 elements per lane (4-bit codes, stochastic rounding)
+#define SDP4_K1_WAVES_32 8 // K1 with 32 elements per lane (4-bit codes; rounded K1 with 4-bit codes or groups of 2048)
 #endif
 #ifndef SDP4_E_K1_PLAIN
 #define SDP4_E_K1_PLAIN 16 // K1 without a transform: 16 or 32 elements per lane
@@ -124,7 +124,7 @@
 #define SDP4_K1_SR_BPC 1 // K1 with stochastic rounding, 32 or 64 per lane: one persistent block per compute unit
 #endif
 #ifndef SDP4_K1_BPC
-#define SDP4_K1_BPC -3
+#define SDP4_K1_BPC -3 // K1 with a transform, 16 or 32 elements per lane
 #endif
 
 // Block shapes of the qWD decoder, of the dequantize-reduce with
