@@ -20,7 +20,8 @@ one slice per available core (up to 16), each in its own thread.
 (read-only, write-only and copy yardsticks of the library, the runtime's own
 copy and fill); each kernel's ``vs_rw_additive`` compares it with a kernel
 that moved its reads at the read-only rate and its writes at the write-only
-rate, one after the other.
+rate, one after the other.  ``graph_step`` times the same step recorded once
+into a HIP graph and replayed (informational).
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 20] [--workload c5]
 """
@@ -245,6 +246,7 @@ def main():
     ap.add_argument("--no-standalone", action="store_true")
     ap.add_argument("--no-group-sweep", action="store_true")
     ap.add_argument("--no-ceilings", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
     # overrides of the workload's shape (the recipe of its data stays that of --workload)
     ap.add_argument("--n", type=int, default=None, help="element count of the shard")
     ap.add_argument("--group", type=int, default=None, help="gradient quantization group")
@@ -305,6 +307,28 @@ def main():
     torch.cuda.synchronize()
     copy_gbps = 2 * 4 * cn * 10 / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
     del src, dst
+
+    # the same step recorded once into a HIP graph and replayed: no per-kernel events and no host
+    # launch work inside the timed replays (informational; `value` is the eager step above)
+    graph_ms = None
+    if not args.no_graph:
+        g = torch.cuda.CUDAGraph()
+        gs = torch.cuda.Stream()
+        gs.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(gs):
+            with torch.cuda.graph(g, stream=gs):
+                hp.step()
+        torch.cuda.current_stream().wait_stream(gs)
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        tg = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - tg) * 1e3 / args.steps
+        del g
+        log(f"{args.steps} graph replays of the step: {graph_ms:.3f} ms/step")
 
     info = hp.kernel_info()
     kernels = {}
@@ -508,6 +532,11 @@ def main():
         "copy_GBps": round(copy_gbps, 1),
         "step_alg_GBps": round(sum(k.alg_bytes for k in info.values()) / (ms_step * 1e-3) / 1e9, 1),
     }
+    if graph_ms is not None:
+        line["graph_step"] = {"ms_per_step": round(graph_ms, 4),
+                              "value": round(fp32_total / (graph_ms * 1e-3) / 1e9, 1),
+                              "note": "the same step recorded once into a HIP graph and replayed, without "
+                                      "per-kernel events; informational, value above is the eager step"}
     if unfused:
         line["hadamard_fusion"] = unfused
     if variants:
