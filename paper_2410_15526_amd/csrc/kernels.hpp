@@ -146,7 +146,7 @@
 #define SDP4_RQ8_WAVES 8
 #endif
 #ifndef SDP4_RQ8_BPC
-#define SDP4_RQ8_BPC -2
+#define SDP4_RQ8_BPC -3
 #endif
 #ifndef SDP4_RQ8_SR_WAVES // ... the same with stochastic rounding
 #define SDP4_RQ8_SR_WAVES 8
