@@ -42,7 +42,7 @@ struct GradQuant {
         }
         constexpr int WPB = kK1Waves32;
         auto k = bits == 8 ? k_grad_quant<8, 32, NB, kDepth, WPB> : k_grad_quant<4, 32, NB, kDepth, WPB>;
-        return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap, s, x, n, group, cn, codes, scale, uint64_t(0),
+        return launch<WPB>(k, wave_blocks<WPB>(n, 32), kK1Cap32, s, x, n, group, cn, codes, scale, uint64_t(0),
                            uint64_t(0));
     }
 };

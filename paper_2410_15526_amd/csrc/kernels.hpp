@@ -91,7 +91,7 @@
 #define SDP4_ENC_STREAM_BPC -4 // the streaming encoder (launches that are not phased), without the phased LDS buffers
 #endif
 #ifndef SDP4_K1_WAVES
-#define SDP4_K1_WAVES 8 // K1 with 16 elements per lane
+#define SDP4_K1_WAVES 4 // K1 with 16 elements per lane
 #endif
 #ifndef SDP4_K1_WAVES_8
 #define SDP4_K1_WAVES_8 4 // K1 with 8 elements per lane
@@ -124,7 +124,10 @@
 #define SDP4_K1_SR_BPC 1 // K1 with stochastic rounding, 32 or 64 per lane: one persistent block per compute unit
 #endif
 #ifndef SDP4_K1_BPC
-#define SDP4_K1_BPC -3 // K1 with a transform, 16 or 32 elements per lane
+#define SDP4_K1_BPC -5 // K1 with a transform, 16 elements per lane
+#endif
+#ifndef SDP4_K1_BPC_32
+#define SDP4_K1_BPC_32 -3 // ... 32 elements per lane
 #endif
 
 // Block shapes of the qWD decoder, of the dequantize-reduce with
@@ -910,7 +913,7 @@ int64_t wave_blocks(int64_t n, int E)
 
 constexpr int kCap = SDP4_BLOCKS_PER_CU;
 constexpr int kEncWaves = SDP4_ENC_WAVES, kEncCap = SDP4_ENC_BPC, kEncStreamCap = SDP4_ENC_STREAM_BPC;
-constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC;
+constexpr int kK1Waves = SDP4_K1_WAVES, kK1Waves32 = SDP4_K1_WAVES_32, kK1Cap = SDP4_K1_BPC, kK1Cap32 = SDP4_K1_BPC_32;
 constexpr int kK1SrCap = SDP4_K1_SR_BPC, kK1Sr16Waves = SDP4_K1_SR16_WAVES, kK1Sr16Cap = SDP4_K1_SR16_BPC;
 constexpr int kK1Waves8 = SDP4_K1_WAVES_8, kK1Cap8 = SDP4_K1_BPC_8;
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN, kK1PlainCap = SDP4_K1_PLAIN_BPC;
