@@ -68,13 +68,14 @@ template <int E>
 int qwd_decode_e(const uint8_t *codes, const float *scale, const float *minv, int64_t n, int group,
                  void *w_prev, bool bf16, bool sym, hipStream_t s)
 {
-    constexpr int WPB = kDecWaves;
     if (bf16) {
+        constexpr int WPB = kDecWaves;
         auto k = sym ? k_qwd_decode<true, true, E, kDepth, WPB> : k_qwd_decode<true, false, E, kDepth, WPB>;
         return launch<WPB>(k, wave_blocks<WPB>(n, E), kDecCap, s, codes, scale, minv, n, group, w_prev);
     }
+    constexpr int WPB = kDecF32Waves;
     auto k = sym ? k_qwd_decode<false, true, E, kDepth, WPB> : k_qwd_decode<false, false, E, kDepth, WPB>;
-    return launch<WPB>(k, wave_blocks<WPB>(n, E), kDecCap, s, codes, scale, minv, n, group, w_prev);
+    return launch<WPB>(k, wave_blocks<WPB>(n, E), kDecF32Cap, s, codes, scale, minv, n, group, w_prev);
 }
 
 } // namespace

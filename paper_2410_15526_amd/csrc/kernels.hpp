@@ -134,10 +134,16 @@
 // re-quantization (K2; 8-bit messages with 16 elements per lane have their
 // own) and of the dequantize-reduce to float32 (K3).
 #ifndef SDP4_DEC_WAVES
-#define SDP4_DEC_WAVES 4
+#define SDP4_DEC_WAVES 2 // qWD decode, bf16 model weights
 #endif
 #ifndef SDP4_DEC_BPC
-#define SDP4_DEC_BPC -4
+#define SDP4_DEC_BPC -8
+#endif
+#ifndef SDP4_DEC_F32_WAVES
+#define SDP4_DEC_F32_WAVES 4 // qWD decode, float32 model weights
+#endif
+#ifndef SDP4_DEC_F32_BPC
+#define SDP4_DEC_F32_BPC -4
 #endif
 #ifndef SDP4_RQ_WAVES
 #define SDP4_RQ_WAVES 4
@@ -919,6 +925,7 @@ constexpr int kK1Waves8 = SDP4_K1_WAVES_8, kK1Cap8 = SDP4_K1_BPC_8;
 constexpr int kK1PlainWaves = SDP4_K1_WAVES_PLAIN, kK1PlainCap = SDP4_K1_PLAIN_BPC;
 constexpr int kHadCap = SDP4_HAD_BPC;
 constexpr int kDecWaves = SDP4_DEC_WAVES, kDecCap = SDP4_DEC_BPC;
+constexpr int kDecF32Waves = SDP4_DEC_F32_WAVES, kDecF32Cap = SDP4_DEC_F32_BPC;
 constexpr int kRqWaves = SDP4_RQ_WAVES, kRqCap = SDP4_RQ_BPC, kRfWaves = SDP4_RF_WAVES, kRfCap = SDP4_RF_BPC;
 constexpr int kRq8Waves = SDP4_RQ8_WAVES, kRq8Cap = SDP4_RQ8_BPC, kRq8SrWaves = SDP4_RQ8_SR_WAVES, kRq8SrCap = SDP4_RQ8_SR_BPC;
 
