@@ -140,10 +140,10 @@
 #define SDP4_DEC_BPC -8
 #endif
 #ifndef SDP4_DEC_F32_WAVES
-#define SDP4_DEC_F32_WAVES 4 // qWD decode, float32 model weights
+#define SDP4_DEC_F32_WAVES 2 // qWD decode, float32 model weights
 #endif
 #ifndef SDP4_DEC_F32_BPC
-#define SDP4_DEC_F32_BPC -4
+#define SDP4_DEC_F32_BPC -8
 #endif
 #ifndef SDP4_RQ_WAVES
 #define SDP4_RQ_WAVES 4
