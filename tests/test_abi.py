@@ -338,3 +338,20 @@ def test_binding_refuses_tensors_too_small_for_the_call(monkeypatch):
     with pytest.raises(ValueError, match=r"xs\[1\]"):
         sdp4.sdp4_reduce_f32([T(4 * n, 4, True), T(4 * n - 4, 4, True)], T(4 * n, 4, True))
     assert calls == ["sdp4_qwd_encode", "sdp4_grad_quant", "sdp4_dequant_reduce"]
+
+
+def test_readme_c_example_compiles(tmp_path):
+    """The C example in README.md uses the header's entry points with their
+    documented signatures: it compiles against include/sdp4.h."""
+    import re
+    import shutil
+    hip_inc = "/opt/rocm/include"
+    if not shutil.which("g++") or not os.path.isdir(os.path.join(hip_inc, "hip")):
+        pytest.skip("g++ or the HIP headers not available")
+    text = open(os.path.join(ROOT, "README.md")).read()
+    m = re.search(r"```c\n(.*?)```", text, re.S)
+    assert m, "README.md has no C example"
+    src = tmp_path / "readme_example.cpp"
+    src.write_text(m.group(1))
+    subprocess.run(["g++", "-std=c++17", "-fsyntax-only", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I", hip_inc,
+                    "-I", os.path.join(ROOT, "include"), str(src)], check=True, capture_output=True)
